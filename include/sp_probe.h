@@ -1,0 +1,196 @@
+/*
+ * sp_probe.h — C ABI of the MI355X (gfx950) Speculative Probing classification forward.
+ *
+ * The operation (Sec. 3.2 "Speculative Probing", Sec. 3.3 Eq. 1-3 of the paper):
+ * for every sequence b of a batch, whose speculative head (MTP / Eagle3, one
+ * decoder layer) already holds the keys and values of the N_b committed tokens
+ * in device memory, append k learned soft-prompt vectors at positions
+ * N_b .. N_b+k-1 and run the frozen layer over those k rows only:
+ *     RMSNorm -> Q/K/V projection -> RoPE -> attention of the k soft queries
+ *     over [cached K/V ; the k new K/V] (causal among the new rows) ->
+ *     o-projection + residual -> RMSNorm -> SwiGLU MLP + residual ->
+ *     final RMSNorm -> read-out row(s) -> linear classifier -> logits[b, 0..C-1].
+ * The new rows' keys and values live in a library-owned scratch area and are
+ * never written into the caller's cache (Sec. 3.3, last paragraph).
+ *
+ * Conventions
+ *  - Every pointer named "device" is a device address on the current HIP
+ *    device; every other pointer is host memory read during the call only.
+ *  - Matrices are row-major [out, in] (a row per output feature).
+ *  - All calls return sp_status and never abort or throw.  Checks that can be
+ *    made on the host run before anything is enqueued: on error no work is
+ *    queued and the outputs are untouched.
+ *  - sp_probe_forward enqueues work on `stream` (a hipStream_t; NULL = the
+ *    null stream) and returns without waiting; it allocates nothing and never
+ *    synchronises the host unless a debug/profiling call below says so.
+ *  - One handle carries one workspace: forwards on the same handle must be
+ *    ordered (same stream, or caller-synchronised).  Distinct handles are
+ *    independent.
+ */
+#ifndef SP_PROBE_H
+#define SP_PROBE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sp_status {
+  SP_OK = 0,
+  SP_ERR_INVALID_ARG = -1,   /* null pointer, bad size, stride or alignment */
+  SP_ERR_UNSUPPORTED = -2,   /* valid but not implemented (e.g. head_dim 96) */
+  SP_ERR_NO_DEVICE = -3,     /* no HIP device, or the current device is not gfx950 */
+  SP_ERR_OUT_OF_MEMORY = -4, /* workspace allocation failed at init */
+  SP_ERR_HIP = -5,           /* a HIP runtime call or kernel launch failed */
+  SP_ERR_CAPACITY = -6,      /* batch larger than max_batch of the handle */
+  SP_ERR_DEVICE_DATA = -7    /* debug mode: device-resident seq_lens / block ids invalid */
+} sp_status;
+
+typedef enum sp_dtype {
+  SP_F32 = 0,   /* fp32 weights, soft prompt and KV cache; fp32 arithmetic throughout */
+  SP_BF16 = 1   /* bf16 storage; bf16 MFMA operands with fp32 accumulation, fp32 norms,
+                   softmax statistics, residual stream and logits */
+} sp_dtype;
+
+typedef enum sp_pool {
+  SP_POOL_LAST = 0,  /* classify the final-normed hidden state of the last soft row
+                        (the read-out of the k-th step, Sec. 3.2) */
+  SP_POOL_MEAN = 1   /* mean of the final-normed hidden states of the k soft rows
+                        (the "pooled final hidden state" of the Fig. 2 caption) */
+} sp_pool;
+
+enum {
+  SP_FLAG_DEBUG = 1,    /* validate device-resident seq_lens and block ids on every forward;
+                           kernels then skip work after a failed check */
+  SP_FLAG_PROFILE = 2   /* record HIP events around every stage of each forward */
+};
+
+/* Shape of the frozen head and limits of a handle. */
+typedef struct sp_probe_config {
+  int32_t hidden;        /* d: multiple of 64 (bf16) or of 4 (f32) */
+  int32_t n_q_heads;     /* query heads */
+  int32_t n_kv_heads;    /* KV heads; n_q_heads % n_kv_heads == 0 (grouped-query attention,
+                            query head h reads KV head h / (n_q_heads / n_kv_heads)) */
+  int32_t head_dim;      /* 64 or 128 */
+  int32_t intermediate;  /* SwiGLU width: multiple of 64 (bf16) or of 4 (f32) */
+  int32_t k;             /* soft-prompt rows per sequence, 1..64 */
+  int32_t n_classes;     /* C, 1..64 */
+  int32_t dtype;         /* sp_dtype */
+  int32_t pool;          /* sp_pool */
+  float rms_eps;         /* epsilon inside every RMSNorm square root */
+  double rope_base;      /* RoPE base; pair (i, i + head_dim/2) turns by pos * base^(-2i/head_dim) */
+  int32_t max_batch;     /* largest batch a forward may pass */
+  int32_t max_seq_len;   /* largest context length N_b a forward may pass (debug mode checks it;
+                            otherwise larger values are clamped to it) */
+  int32_t split_len;     /* tokens per attention split, a power of two >= 256; 0 = automatic */
+  int32_t flags;         /* SP_FLAG_* */
+} sp_probe_config;
+
+/* The head's resident KV cache (Sec. 3.3 Eq. 2-3: K_{1:n}, V_{1:n}), read-only.
+ *
+ * Storage is paged: sequence b's token t lives in logical block t / block_size
+ * of that sequence, at slot t % block_size.  The physical block is
+ * block_table[b * max_blocks_per_seq + t / block_size], or, when block_table is
+ * NULL ("contiguous"), b * max_blocks_per_seq + t / block_size.
+ * Inside physical block p, KV head g, with x = 16 / sizeof(element) (8 for bf16,
+ * 4 for f32) and the cached keys post-RoPE:
+ *   K(t, i) = k_base[p*k_stride_block + g*k_stride_head + ((i / x) * block_size + t) * x + i % x]
+ *   V(t, i) = v_base[p*v_stride_block + g*v_stride_head + i * block_size + t]
+ * (t = slot in block, i = 0..head_dim-1).  Strides are in elements.  Only
+ * slots t < N_b of a sequence are read as data; other slots may hold anything,
+ * including NaN.  Pointers and strides must be 16-byte aligned. */
+typedef struct sp_kv_cache {
+  const void* k_base;          /* device */
+  const void* v_base;          /* device */
+  int64_t num_blocks;          /* physical blocks in the pool (debug-mode bound for block ids) */
+  int64_t k_stride_block, k_stride_head;
+  int64_t v_stride_block, v_stride_head;
+  int32_t block_size;          /* tokens per block: a power of two >= 16 */
+  int32_t max_blocks_per_seq;  /* row length of block_table; >= ceil(N_b / block_size) */
+  int32_t batch;               /* B, number of sequences; 0 is a no-op */
+} sp_kv_cache;
+
+/* Frozen head weights and the task's classifier, all device pointers in the
+ * config's dtype except b_cls (fp32), 16-byte aligned, [out, in] row-major:
+ *   in_norm[d], w_q[n_q*hd][d], w_k[n_kv*hd][d], w_v[n_kv*hd][d], w_o[d][n_q*hd],
+ *   post_norm[d], w_gate[I][d], w_up[I][d], w_down[d][I], final_norm[d],
+ *   w_cls[C][d], b_cls[C] (nullable: no bias). */
+typedef struct sp_probe_weights {
+  const void* in_norm;
+  const void* w_q;
+  const void* w_k;
+  const void* w_v;
+  const void* w_o;
+  const void* post_norm;
+  const void* w_gate;
+  const void* w_up;
+  const void* w_down;
+  const void* final_norm;
+  const void* w_cls;
+  const float* b_cls;
+} sp_probe_weights;
+
+typedef struct sp_probe sp_probe_t;  /* opaque handle, library-owned */
+
+/* Bytes of device workspace a handle with this config allocates (0 if invalid). */
+size_t sp_probe_workspace_bytes(const sp_probe_config* cfg);
+
+/* Validate cfg, check that the current HIP device is gfx950, allocate the
+ * workspace (soft-row scratch K/V, queries, split partials, activations) for
+ * max_batch x max_seq_len and return a handle in *out.  The only allocating call. */
+int sp_probe_init(const sp_probe_config* cfg, sp_probe_t** out);
+
+/* The classification forward (Sec. 3.2-3.3) for kv_cache->batch sequences.
+ *   seq_lens    device int32[B]: committed-prefix length N_b of each sequence (may be 0)
+ *   block_table device int32[B * max_blocks_per_seq] or NULL (contiguous storage)
+ *   soft_prompt device [k][d]: the task's soft-prompt vectors, row j at position N_b + j
+ *   weights     frozen head + classifier (host struct of device pointers)
+ *   logits      device fp32 [B][C], written; raw scores before any sigmoid/softmax
+ *   stream      hipStream_t
+ * Device-resident seq_lens and block ids are trusted unless SP_FLAG_DEBUG is set. */
+int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv_cache, const int32_t* seq_lens,
+                     const int32_t* block_table, const void* soft_prompt,
+                     const sp_probe_weights* weights, float* logits, void* stream);
+
+/* Free the workspace and the handle (waits for the device). NULL is accepted. */
+int sp_probe_destroy(sp_probe_t* h);
+
+/* Human-readable name of a status code (static string). */
+const char* sp_probe_status_string(int status);
+
+/* Intermediate values of the last forward, for tests.  tap selects:
+ *   SP_TAP_QKV   fp32 [k][(n_q + 2 n_kv) hd]   projections of the normed soft rows
+ *   SP_TAP_ATTN  dtype [B k][n_q hd]           attention output, row b*k + j
+ *   SP_TAP_A     fp32 [B k][d]                 residual after the o-projection
+ *   SP_TAP_Y     fp32 [B k][d]                 residual after the MLP
+ * sp_probe_tap_bytes returns the size for a batch; sp_probe_copy_tap enqueues a
+ * device-to-device copy of it into dst (device, dst_bytes >= that size). */
+enum { SP_TAP_QKV = 0, SP_TAP_ATTN = 1, SP_TAP_A = 2, SP_TAP_Y = 3 };
+size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch);
+int sp_probe_copy_tap(sp_probe_t* h, int tap, int32_t batch, void* dst, size_t dst_bytes, void* stream);
+
+/* Debug mode: wait for `stream`, then report SP_ERR_DEVICE_DATA if any forward
+ * since the last call saw an invalid seq_len or block id (and clear the flag). */
+int sp_probe_check_device_error(sp_probe_t* h, void* stream);
+
+/* Profiling mode: per-stage device time summed over the forwards since the last
+ * read (waits for them).  Stages, in order: 0 soft-row prep (norm, QKV, RoPE),
+ * 1 split attention, 2 split merge, 3 o-projection, 4 post-attention norm,
+ * 5 gate/up + SwiGLU, 6 down projection, 7 final norm + classifier.
+ * stage_ms[n_stages] receives milliseconds, *n_forwards the number of forwards
+ * counted (at most the last 256). */
+#define SP_N_STAGES 8
+int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stages, int32_t* n_forwards);
+
+/* Split plan of a handle: tokens per attention split and the launch grid of
+ * the split-attention kernel for a batch (for measurement and tests). */
+int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len, int32_t* max_splits,
+                  int32_t* rows_per_kv_head, int32_t* query_groups);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SP_PROBE_H */

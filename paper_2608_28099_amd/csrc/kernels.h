@@ -1,0 +1,102 @@
+// Internal interface between the host runtime and the kernels (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sp {
+
+enum DType { kF32 = 0, kBF16 = 1 };
+
+// ---------------------------------------------------------------- soft-row prep
+// out[r][i] = x[r][i] / sqrt(mean_i x[r][i]^2 + eps) * gain[i], rows r < rows.
+hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const void* x,
+                               const void* gain, void* out, int rows, int d, float eps,
+                               hipStream_t s);
+
+struct RopeParams {
+  const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32
+  const int* seq_lens;     // device [B]
+  const int* err;          // nullable: skip everything if *err != 0
+  void* q;                 // [B][n_kv][r_alloc][hd]           (compute dtype), scaled
+  void* k_soft;            // [B][n_kv] tiles of ks tokens, chunked layout (x = 16 B / elem)
+  void* v_soft;            // [n_kv][hd][ks] (batch-invariant)
+  int n_q, n_kv, hd, k, group, r_alloc, ks, max_seq_len;
+  double rope_base;
+  float q_scale;           // log2(e) / sqrt(hd)
+};
+hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnParams {
+  const void* q;           // [B][n_kv][r_alloc][hd], pre-scaled by log2(e)/sqrt(hd)
+  const void* k_soft;      // [B][n_kv] chunked tiles of ks tokens
+  const void* v_soft;      // [n_kv][hd][ks]
+  const void* k_base;
+  const void* v_base;
+  int64_t k_sb, k_sh, v_sb, v_sh;     // elements
+  const int* block_table;  // nullable (contiguous)
+  const int* seq_lens;
+  const int* err;          // nullable
+  float* o_part;           // [B][n_kv][max_splits][r_alloc][hd] fp32, unnormalised
+  float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
+  int n_kv, group, k, rows, r_alloc, ks, n_qgroups;
+  int bs_log2, mbps, max_seq_len, split_len, max_splits;
+};
+// bf16 MFMA path: head_dim 64/128, rows per wave 16*qt.
+hipError_t launch_attention_bf16(const AttnParams& p, int hd, int qt, int batch, hipStream_t s);
+// fp32 VALU path: head_dim 64/128, rows <= 64.
+hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);
+
+struct MergeParams {
+  const float* o_part;
+  const float2* ml_part;
+  const int* seq_lens;
+  const int* err;
+  void* out;               // [B k][n_q hd] (compute dtype)
+  int n_kv, group, k, rows, r_alloc, hd, max_splits, split_len, max_seq_len, n_q;
+};
+hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM
+enum Epilogue {
+  kEpiStore = 0,      // C fp32 = acc
+  kEpiResidRow = 1,   // C fp32 = acc + R[m % r_mod][n]   (R in the compute dtype)
+  kEpiResidF32 = 2,   // C fp32 = acc + R[m][n]           (R fp32, ld = ldc)
+  kEpiSwiglu = 3      // C (compute dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
+};
+struct GemmParams {
+  const void* a;           // [M][lda]
+  const void* b[3];        // weight row blocks: rows [0, b_split0) from b[0], [b_split0, b_split1)
+                           // from b[1], the rest from b[2]; SwiGLU: b[0] gate, b[1] up
+  int b_split0, b_split1;
+  int ldb;                 // row stride of every b[i]
+  void* c;
+  const void* r;           // residual
+  int M, N, K, lda, ldc, r_mod;
+};
+hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s);
+
+// ---------------------------------------------------------------- read-out
+struct ClsParams {
+  const float* y;          // [B k][d]
+  const void* final_norm;  // [d]
+  const void* w_cls;       // [C][d]
+  const float* b_cls;      // nullable
+  float* logits;           // [B][C]
+  int k, d, n_classes, pool_mean;
+  float eps;
+};
+hipError_t launch_final_classifier(DType dt, const ClsParams& p, int batch, hipStream_t s);
+
+// ---------------------------------------------------------------- debug validation
+struct ValidateParams {
+  const int* seq_lens;
+  const int* block_table;  // nullable
+  int* err;
+  int64_t num_blocks;
+  int mbps, bs_log2, max_seq_len;
+};
+hipError_t launch_validate(const ValidateParams& p, int batch, hipStream_t s);
+
+}  // namespace sp

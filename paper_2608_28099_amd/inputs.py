@@ -10,8 +10,10 @@ returns the same bytes.
 KV cache storage (the boundary's paged layout).  The pool is one tensor
 ``pool[num_blocks, n_kv, 2, block_size * head_dim]``.  For block ``p`` and KV
 head ``g``:
-  * ``pool[p, g, 0]`` is the K tile, token-major: element (t, i) at ``t*head_dim + i``;
-  * ``pool[p, g, 1]`` is the V tile, dim-major:   element (t, i) at ``i*block_size + t``.
+  * ``pool[p, g, 0]`` is the K tile in 16-byte chunks of the head dimension:
+    element (t, i) at ``((i // x) * block_size + t) * x + i % x`` with
+    x = 16 / element size (8 for bf16, 4 for fp32);
+  * ``pool[p, g, 1]`` is the V tile, dim-major: element (t, i) at ``i*block_size + t``.
 Token slots past a sequence's length and every spare block are filled with NaN,
 so any read of them that reaches an output shows up as NaN.
 """
@@ -137,6 +139,10 @@ class KVCache:
                                 device=self.pool.device)
         return self.block_table[b].long()
 
+    @property
+    def x(self) -> int:
+        return 16 // self.pool.element_size()
+
     def logical_kv(self, b: int):
         """(K, V) of sequence b as dense [n_kv, N_b, head_dim] tensors on the pool's device."""
         n = int(self.seq_lens[b])
@@ -144,7 +150,9 @@ class KVCache:
         blocks = self.physical_blocks(b)[:nblk]
         tiles = self.pool.index_select(0, blocks)            # [nblk, n_kv, 2, bs*hd]
         bs, hd = self.block_size, self.head_dim
-        k = tiles[:, :, 0].reshape(nblk, self.n_kv, bs, hd)
+        x = self.x
+        k = tiles[:, :, 0].reshape(nblk, self.n_kv, hd // x, bs, x).permute(0, 1, 3, 2, 4)
+        k = k.reshape(nblk, self.n_kv, bs, hd)
         v = tiles[:, :, 1].reshape(nblk, self.n_kv, hd, bs).transpose(2, 3)
         k = k.permute(1, 0, 2, 3).reshape(self.n_kv, nblk * bs, hd)[:, :n]
         v = v.permute(1, 0, 2, 3).reshape(self.n_kv, nblk * bs, hd)[:, :n]
@@ -153,9 +161,10 @@ class KVCache:
 
 def _poison_tail(pool: torch.Tensor, blk: int, used: int, bs: int, hd: int) -> None:
     n_kv = pool.shape[1]
-    kt = pool[blk, :, 0].view(n_kv, bs, hd)
+    x = 16 // pool.element_size()
+    kt = pool[blk, :, 0].view(n_kv, hd // x, bs, x)
     vt = pool[blk, :, 1].view(n_kv, hd, bs)
-    kt[:, used:, :] = float("nan")
+    kt[:, :, used:, :] = float("nan")
     vt[:, :, used:] = float("nan")
 
 
@@ -266,7 +275,9 @@ def repack(kv: KVCache, layout: str, block_size: Optional[int] = None, perm_seed
         vp[:, :n] = v
         for j in range(npad // bs):
             p = int(bt[b, j])
-            pool[p, :, 0] = kp[:, j * bs:(j + 1) * bs].reshape(n_kv, bs * hd)
+            x = 16 // pool.element_size()
+            kt = kp[:, j * bs:(j + 1) * bs].reshape(n_kv, bs, hd // x, x).permute(0, 2, 1, 3)
+            pool[p, :, 0] = kt.reshape(n_kv, bs * hd)
             pool[p, :, 1] = vp[:, j * bs:(j + 1) * bs].transpose(1, 2).reshape(n_kv, bs * hd)
     return KVCache(pool=pool, block_table=None if layout == "contiguous" else bt.to(dev),
                    seq_lens=kv.seq_lens.clone(), block_size=bs, max_blocks_per_seq=mbps,

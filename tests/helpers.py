@@ -1,0 +1,58 @@
+"""Shared test helpers: moving generated inputs to the GPU and running the oracle
+on the same bytes."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from oracle import probe as oracle
+from paper_2608_28099_amd import inputs
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}    # max-abs logits tolerance per storage dtype
+ARGMAX_MARGIN = 5e-2                  # argmax must agree where the oracle's top-2 gap exceeds this
+
+
+def to_device(kv: inputs.KVCache, params: dict, dev):
+    kv_d = inputs.KVCache(kv.pool.to(dev), None if kv.block_table is None else kv.block_table.to(dev),
+                          kv.seq_lens.to(dev), kv.block_size, kv.max_blocks_per_seq, kv.n_kv,
+                          kv.head_dim)
+    p_d = {k: (None if v is None else v.to(dev)) for k, v in params.items()}
+    return kv_d, p_d
+
+
+def oracle_weights(params: dict) -> dict:
+    return {k: (None if v is None else v.detach().double().cpu().numpy())
+            for k, v in params.items() if k != "soft_prompt"}
+
+
+def head_shape(w) -> oracle.HeadShape:
+    return oracle.HeadShape(w.n_q_heads, w.n_kv_heads, w.head_dim, w.rms_eps, w.rope_base, w.pool)
+
+
+def oracle_outputs(w, kv: inputs.KVCache, params: dict, batch_idx, W=None):
+    """Oracle results (dicts with logits and taps) for the sequences in batch_idx,
+    computed from the exact stored values of `kv` and `params` (any device)."""
+    W = W if W is not None else oracle_weights(params)
+    soft = params["soft_prompt"].detach().double().cpu().numpy()
+    shape = head_shape(w)
+    outs = []
+    for b in batch_idx:
+        k, v = kv.logical_kv(b)
+        outs.append(oracle.probe_sequence(k.double().cpu().numpy(), v.double().cpu().numpy(), soft,
+                                          W, shape))
+    return outs
+
+
+def check_logits(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -> float:
+    """The parity bar: max-abs within TOL[dtype]; identical argmax where the
+    oracle's top-2 margin exceeds ARGMAX_MARGIN.  Returns the max error."""
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite logits"
+    err = float(np.max(np.abs(got - ref))) if got.size else 0.0
+    assert err <= TOL[dtype], f"{what}: max|gpu - oracle| = {err:.3e} > {TOL[dtype]}"
+    if ref.shape[1] >= 2:
+        srt = np.sort(ref, axis=1)
+        decisive = (srt[:, -1] - srt[:, -2]) > ARGMAX_MARGIN
+        assert np.array_equal(np.argmax(got, 1)[decisive], np.argmax(ref, 1)[decisive]), \
+            f"{what}: argmax differs on a decisive row"
+    return err

@@ -1,0 +1,247 @@
+"""GPU parity of the HIP probe forward against the fp64 oracle, through the C ABI.
+
+Small workloads: every sequence, every logit, plus intermediate taps.  Full-size
+workloads (the shapes the benchmark runs, same launch configuration): sampled
+sequences the oracle recomputes one by one.  Invariances that must hold bit for
+bit: batch order, block placement, contiguous vs paged storage, repeated runs.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_28099_amd import binding, configs, inputs
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [configs.TINY_F32, configs.TINY_PEAKY_F32, configs.TINY_RAGGED_F32, configs.SMALL_BF16,
+         configs.SMALL_G5_BF16]
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    binding.load()
+    return torch.device("cuda:0")
+
+
+def small_case(w, dev, layout=None, block_size=None):
+    lens = inputs.seq_lens(w)
+    kv = inputs.kv_cache(w, lens, "cpu", layout=layout, block_size=block_size)
+    params = inputs.params(w, "cpu")
+    kv_d, p_d = H.to_device(kv, params, dev)
+    return kv, params, kv_d, p_d
+
+
+def announce(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
+def test_small_logits_match_oracle(w, dev):
+    announce(f"[parity] {w.name}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    err = H.check_logits(got, ref, w.dtype, w.name)
+    announce(f"[parity] {w.name}: max err {err:.3e}")
+    probe.close()
+
+
+@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
+def test_small_taps_match_oracle(w, dev):
+    """Stage-wise: Q/K/V projections, attention output, residuals a and y."""
+    announce(f"[taps] {w.name}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    probe.forward(kv_d, p_d)
+    B, k, d = w.batch, w.k, w.hidden
+    dt = inputs.TORCH_DTYPE[w.dtype]
+    outs = H.oracle_outputs(w, kv, params, range(B))
+    qkv = probe.tap(binding.SP_TAP_QKV, B, dev).view(torch.float32).cpu().double().numpy()
+    attn = probe.tap(binding.SP_TAP_ATTN, B, dev).view(dt).cpu().double().numpy()
+    a = probe.tap(binding.SP_TAP_A, B, dev).view(torch.float32).cpu().double().numpy()
+    y = probe.tap(binding.SP_TAP_Y, B, dev).view(torch.float32).cpu().double().numpy()
+    probe.close()
+    W = H.oracle_weights(params)
+    from oracle import probe as oracle
+    u = oracle.rms_norm(params["soft_prompt"].double().numpy(), W["in_norm"], w.rms_eps)
+    qkv_ref = np.concatenate([u @ W["w_q"].T, u @ W["w_k"].T, u @ W["w_v"].T], axis=1)
+    # relative to the magnitude of each tensor: fp32 path ~1e-6, bf16 path ~1e-2
+    rel = 1e-4 if w.dtype == "f32" else 3e-2
+
+    def close(x, r, what):
+        scale = max(np.max(np.abs(r)), 1e-30)
+        e = np.max(np.abs(x - r)) / scale
+        assert e <= rel, f"{w.name} {what}: relative error {e:.3e}"
+
+    close(qkv.reshape(k, -1), qkv_ref, "qkv")
+    attn = attn.reshape(B, k, -1)
+    for b in range(B):
+        close(attn[b], outs[b]["o"], f"attention b={b}")
+        close(a.reshape(B, k, d)[b], outs[b]["a"], f"a b={b}")
+        close(y.reshape(B, k, d)[b], outs[b]["y"], f"y b={b}")
+
+
+def test_mean_pool_and_bias(dev):
+    w = configs.SMALL_BF16.replace(name="small_bf16_mean_bias", pool="mean", cls_bias=True, seed=21)
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, w.name)
+    probe.close()
+
+
+@pytest.mark.parametrize("k", [1, 2, 17, 33, 64])
+def test_soft_row_counts(k, dev):
+    """k = 1 (SP-1), odd k crossing 16- and 32-row boundaries, and the maximum 64."""
+    w = configs.SMALL_BF16.replace(name=f"small_k{k}", k=k, seed=30 + k)
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, w.name)
+    probe.close()
+
+
+@pytest.mark.parametrize("hd", [64, 128])
+def test_head_dims_and_splits(hd, dev):
+    """Several splits per sequence (split_len 256), head_dim 64 and 128, both dtypes."""
+    for dtype in ("bf16", "f32"):
+        w = configs.Workload(name=f"splits_{dtype}_{hd}", dtype=dtype, batch=3, k=3, hidden=256,
+                             n_q_heads=4, n_kv_heads=2, head_dim=hd, intermediate=320, n_classes=2,
+                             seq_len=("list", (700, 256, 1)), kv_std=1.0, weight_std=0.05, seed=40)
+        kv, params, kv_d, p_d = small_case(w, dev)
+        probe = binding.Probe(w, split_len=256)
+        assert probe.plan(w.batch)["max_splits"] == 3
+        got = probe.forward(kv_d, p_d).cpu().numpy()
+        ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+        H.check_logits(got, ref, w.dtype, w.name)
+        probe.close()
+
+
+# ---------------------------------------------------------------- invariances (bitwise)
+
+def test_invariances_are_bitwise(dev):
+    w = configs.SMALL_BF16
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    base = probe.forward(kv_d, p_d).clone()
+    again = probe.forward(kv_d, p_d).clone()
+    assert torch.equal(base, again), "two identical runs differ"
+    # block placement and block size
+    for layout, bs, seed in (("paged", 16, 5), ("paged", 32, 6), ("contiguous", None, 0)):
+        kv2 = inputs.repack(kv, layout, bs, perm_seed=seed)
+        kv2_d, _ = H.to_device(kv2, params, dev)
+        probe2 = binding.Probe(w, max_seq_len=w.max_seq_len())
+        out = probe2.forward(kv2_d, p_d)
+        assert torch.equal(out, base), f"{layout} bs={bs} differs"
+        probe2.close()
+    # batch order
+    perm = [3, 0, 4, 2, 1]
+    kvp = inputs.permute_batch(kv_d, perm)
+    out = probe.forward(kvp, p_d)
+    assert torch.equal(out, base[perm]), "batch permutation changes the logits"
+    probe.close()
+
+
+def test_kv_cache_is_not_written(dev):
+    """Sec. 3.3: the soft rows' K/V go to scratch; the head's cache is untouched."""
+    w = configs.TINY_RAGGED_F32
+    kv, params, kv_d, p_d = small_case(w, dev)
+    before = kv_d.pool.clone()
+    bt_before = kv_d.block_table.clone()
+    probe = binding.Probe(w)
+    probe.forward(kv_d, p_d)
+    torch.cuda.synchronize()
+    assert torch.equal(kv_d.pool.view(torch.int32), before.view(torch.int32))
+    assert torch.equal(kv_d.block_table, bt_before)
+    probe.close()
+
+
+def test_empty_batch_and_host_errors(dev):
+    w = configs.SMALL_BF16
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    sentinel = torch.full((w.batch, w.n_classes), 123.0, device=dev)
+    stream = torch.cuda.current_stream().cuda_stream
+    wt = binding.make_weights(p_d)
+    # B = 0: no-op
+    st = binding.sp_probe_forward(probe.h, binding.make_kv(kv_d, 0), kv_d.seq_lens.data_ptr(),
+                                  kv_d.block_table.data_ptr(), p_d["soft_prompt"].data_ptr(), wt,
+                                  sentinel.data_ptr(), stream)
+    assert st == 0
+    # batch above capacity, a null weight, a misaligned pointer, a bad block size
+    bad = []
+    kvc = binding.make_kv(kv_d, w.batch + 1)
+    bad.append((kvc, wt, binding.SP_OK - 6))
+    wt_null = binding.make_weights(dict(p_d, w_o=None))
+    bad.append((binding.make_kv(kv_d), wt_null, -1))
+    kvm = binding.make_kv(kv_d)
+    kvm.k_base += 2
+    bad.append((kvm, wt, -1))
+    kvb = binding.make_kv(kv_d)
+    kvb.block_size = 24
+    bad.append((kvb, wt, -1))
+    for kvx, wtx, want in bad:
+        st = binding.sp_probe_forward(probe.h, kvx, kv_d.seq_lens.data_ptr(),
+                                      kv_d.block_table.data_ptr(), p_d["soft_prompt"].data_ptr(),
+                                      wtx, sentinel.data_ptr(), stream)
+        assert st == want, (st, want)
+    torch.cuda.synchronize()
+    assert torch.all(sentinel == 123.0), "logits written despite an error"
+    probe.close()
+
+
+def test_profile_mode_reports_every_stage(dev):
+    w = configs.SMALL_BF16
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w, flags=binding.SP_FLAG_PROFILE)
+    for _ in range(3):
+        probe.forward(kv_d, p_d)
+    stages, n = probe.profile_read()
+    assert n == 3
+    assert all(v > 0 for v in stages.values()), stages
+    probe.close()
+
+
+# ---------------------------------------------------------------- full-size workloads
+
+FULL = [configs.QWEN4B_BF16, configs.QWEN9B_BF16, configs.QWEN27B_BF16, configs.LONG_9B_BF16]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("w", FULL, ids=lambda w: w.name)
+def test_full_size_sampled_sequences(w, dev):
+    """The workload at its full size on the GPU, in the benchmark's launch
+    configuration; the oracle recomputes sampled sequences (shortest, longest,
+    and two seeded picks) one by one."""
+    announce(f"[full] {w.name}: generating on the GPU")
+    lens = inputs.seq_lens(w)
+    kv = inputs.kv_cache(w, lens, dev)
+    params = inputs.params(w, dev)
+    probe = binding.Probe(w)
+    announce(f"[full] {w.name}: plan {probe.plan(w.batch)}")
+    got = probe.forward(kv, params).cpu().numpy()
+    torch.cuda.synchronize()
+    announce(f"[full] {w.name}: forward done")
+    rng = np.random.default_rng(100 + w.seed)
+    pick = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(w.batch, 2, replace=False).tolist()})
+    if os.environ.get("SP_FULL_SAMPLES"):
+        pick = pick[: int(os.environ["SP_FULL_SAMPLES"])]
+    W = H.oracle_weights(params)
+    for b in pick:
+        ref = H.oracle_outputs(w, kv, params, [b], W=W)[0]["logits"]
+        err = H.check_logits(got[b:b + 1], ref[None], w.dtype, f"{w.name} b={b} N={lens[b]}")
+        announce(f"[full] {w.name}: b={b} N={lens[b]} max err {err:.3e}")
+    assert np.all(np.isfinite(got))
+    probe.close()
+    del kv, params
+    torch.cuda.empty_cache()
