@@ -1,0 +1,173 @@
+"""Benchmark of the Speculative Probing classification forward on one MI355X.
+
+One step = one sp_probe_forward over the whole batch of the workload (soft-row
+prep, split attention over the paged KV cache, merge, o-projection, norm,
+SwiGLU MLP, final norm and classifier), inputs already resident in HBM.
+
+Prints one JSON line:
+  value      classifications/s = batch / (wall time per step), timed over K steps
+             bracketed by device synchronisation;
+  roofline   the split-attention kernel (the dominant one on the long-context
+             workload): algorithmic KV bytes per launch / its mean duration,
+             from HIP events recorded on the launch stream around it in the timed
+             steps, against 8 TB/s;
+  cpu_baseline  the fp64 oracle on the host cores over a bounded sample of the
+             same workload's sequences.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "classifications/sec at 1 MI355X; attention KV-read GB/s as % of HBM peak"
+HBM_PEAK_GBPS = 8000.0
+DEFAULT_WORKLOAD = "long_9b_bf16"
+ATTN_SRC = os.path.join(ROOT, "paper_2608_28099_amd", "csrc", "attention.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_long_9b_bf16_traffic.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--split-len", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle sample: sequences are timed until this much CPU time has passed")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain 1 GiB device copy (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def attention_source_hash() -> str:
+    return hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_per_launch():
+    """HBM bytes per attention launch from committed counter runs, if they were
+    taken on the current attention source; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("attention_src_sha256_16") != attention_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, kv, params, seconds: float):
+    """The oracle, as written, timed on the host over whole sequences of the workload."""
+    import numpy as np
+    import threadpoolctl
+
+    from oracle import probe as oracle
+    W = {k: (None if v is None else v.double().cpu().numpy()) for k, v in params.items() if k != "soft_prompt"}
+    soft = params["soft_prompt"].double().cpu().numpy()
+    shape = oracle.HeadShape(w.n_q_heads, w.n_kv_heads, w.head_dim, w.rms_eps, w.rope_base, w.pool)
+    threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
+    done, spent, toks = 0, 0.0, 0
+    for b in range(w.batch):
+        k, v = kv.logical_kv(b)
+        k, v = k.double().cpu().numpy(), v.double().cpu().numpy()
+        t = time.perf_counter()
+        oracle.probe_sequence(k, v, soft, W, shape)
+        spent += time.perf_counter() - t
+        done += 1
+        toks += k.shape[1]
+        del k, v
+        if spent >= seconds:
+            break
+    return {"value": done / spent, "unit": "classifications/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {w.batch} sequences ({toks} context tokens), fp64 numpy, "
+                      f"{spent:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the forward is per-sequence "
+              "independent and shards by sequence, which this build does not run.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_28099_amd import binding, configs, inputs
+
+    dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        n = 1 << 30
+        src = torch.ones(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 3}))
+        return
+
+    w = configs.WORKLOADS.get(args.workload) or configs.STRESS[args.workload]
+    print(f"[bench] {w.name}: generating inputs on the GPU", file=sys.stderr, flush=True)
+    lens = inputs.seq_lens(w)
+    kv = inputs.kv_cache(w, lens, dev)
+    params = inputs.params(w, dev)
+    logits = torch.empty((w.batch, w.n_classes), dtype=torch.float32, device=dev)
+    probe = binding.Probe(w, split_len=args.split_len, flags=binding.SP_FLAG_PROFILE)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        probe.forward(kv, params, logits)
+    torch.cuda.synchronize()
+    probe.profile_read()  # discard warm-up events
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        probe.forward(kv, params, logits)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    stages, n_fwd = probe.profile_read()
+    assert n_fwd == args.steps
+    ms_per_step = 1000.0 * elapsed / args.steps
+    assert bool(torch.isfinite(logits).all()), "non-finite logits"
+
+    esz = 2 if w.dtype == "bf16" else 4
+    kv_bytes = int(lens.astype("int64").sum()) * w.n_kv_heads * w.head_dim * 2 * esz
+    attn_ms = stages["attention"] / n_fwd
+    achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
+    traffic = traffic_per_launch()
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "kernel": "attn_split_bf16" if w.dtype == "bf16" else "attn_split_f32",
+                "algorithmic_bytes_per_launch": kv_bytes, "mean_launch_ms": round(attn_ms, 4)}
+    plan = probe.plan(w.batch)
+    out = {
+        "metric": METRIC, "value": round(w.batch / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded; random-init head weights; paged KV ~N(0,1))",
+        "config": {"workload": w.name, "batch": w.batch, "seq_len": list(w.seq_len), "k": w.k,
+                   "hidden": w.hidden, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
+                   "head_dim": w.head_dim, "intermediate": w.intermediate, "n_classes": w.n_classes,
+                   "kv_layout": w.layout, "block_size": kv.block_size, "kv_bytes": kv_bytes,
+                   "split_len": plan["split_len"], "parallelism": "single GPU"},
+        "roofline": roofline,
+        "attention_gbps": round(achieved, 1),
+        "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},
+    }
+    probe.close()
+    if not args.no_cpu_baseline:
+        print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
