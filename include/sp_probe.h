@@ -50,8 +50,10 @@ typedef enum sp_status {
 
 typedef enum sp_dtype {
   SP_F32 = 0,   /* fp32 weights, soft prompt and KV cache; fp32 arithmetic throughout */
-  SP_BF16 = 1   /* bf16 storage; bf16 MFMA operands with fp32 accumulation, fp32 norms,
-                   softmax statistics, residual stream and logits */
+  SP_BF16 = 1   /* bf16 storage of weights, soft prompt and KV cache; fp16 MFMA operands
+                   (bf16 values converted exactly, activations rounded to fp16) with fp32
+                   accumulation; fp32 norms, softmax statistics, residual stream, logits.
+                   KV and weight magnitudes must stay below 65504 (fp16 range) */
 } sp_dtype;
 
 typedef enum sp_pool {
@@ -162,7 +164,8 @@ const char* sp_probe_status_string(int status);
 
 /* Intermediate values of the last forward, for tests.  tap selects:
  *   SP_TAP_QKV   fp32 [k][(n_q + 2 n_kv) hd]   projections of the normed soft rows
- *   SP_TAP_ATTN  dtype [B k][n_q hd]           attention output, row b*k + j
+ *   SP_TAP_ATTN  [B k][n_q hd]                 attention output, row b*k + j (fp16 for
+ *                                              SP_BF16, fp32 for SP_F32)
  *   SP_TAP_A     fp32 [B k][d]                 residual after the o-projection
  *   SP_TAP_Y     fp32 [B k][d]                 residual after the MLP
  * sp_probe_tap_bytes returns the size for a batch; sp_probe_copy_tap enqueues a

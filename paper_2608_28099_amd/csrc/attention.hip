@@ -10,18 +10,28 @@
 // partial; the merge combines partials with the log-sum-exp rule
 //   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  O = sum_s O_s 2^(m_s - M) / L.
 //
-// bf16 path, per 16-token chunk (always inside one block, so one block-table
-// lookup per chunk, uniform across the wave):
-//   S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with the 16 tokens as MFMA rows:
+// bf16 path (bf16 KV cache, fp16 MFMA operands, fp32 accumulation), per
+// 16-token chunk (always inside one block, so one block-table lookup per chunk,
+// uniform across the wave):
+//   S^T = K Q^T on v_mfma_f32_16x16x32_f16 with the 16 tokens as MFMA rows:
 //   lane (li, la) loads K row li (16-byte pieces of the chunked K tile) and,
 //   after the MFMA, holds the scores of tokens 4la .. 4la+3 for query li.  That
-//   is exactly the A operand of v_mfma_f32_16x16x16_bf16 (query row li, 4
+//   is exactly the A operand of v_mfma_f32_16x16x16_f16 (query row li, 4
 //   consecutive tokens), so P never goes through LDS.
 //   O += P V with V as the B operand: lane (li, la) needs V[4la .. 4la+3][16nt + li],
 //   one 8-byte load from the dim-major V tile; the 16 lanes of a row read 512
-//   contiguous bytes.
+//   contiguous bytes.  K and V are loaded as bf16 with streaming loads and
+//   converted to fp16 in registers (exact for |x| in [2^-14, 65504]); the queries
+//   and the soft rows' K/V arrive in fp16.
+//   All query tiles' QK products are issued before any softmax work, and one
+//   wave-wide test per chunk decides whether a reference max must move, so the
+//   common path is one basic block the scheduler can overlap.
 #include "common.h"
 #include "kernels.h"
+
+#ifndef SP_ATTN_DEPTH
+#define SP_ATTN_DEPTH 3
+#endif
 
 namespace sp {
 namespace {
@@ -41,32 +51,50 @@ template <int HD>
 struct Frag {
   static constexpr int NC = HD / 32;  // 32-wide head-dim chunks (QK contraction)
   static constexpr int NT = HD / 16;  // 16-wide head-dim tiles (PV output)
-  bf16x8 k[NC];                       // K[token li][8 (la*NC + c) .. +7]
+  uint4 k[NC];                        // K[token li][8 (la*NC + c) .. +7]
   uint2 v[NT];                        // V[tokens 4la .. 4la+3][16nt + li]
 };
 
 // kt/vt: K and V tile bases of the block holding the chunk, slot0: slot of the
-// chunk's first token in that block, bs: tile length in tokens.
-template <int HD>
-__device__ __forceinline__ void load_frag(Frag<HD>& f, const bf16* kt, const bf16* vt, int slot0,
-                                          int bs, int li, int la) {
+// chunk's first token in that block, bs: tile length in tokens.  STREAM: the
+// KV cache, read once (non-temporal loads).
+template <int HD, bool STREAM, typename T>
+__device__ __forceinline__ void load_frag(Frag<HD>& f, const T* kt, const T* vt, int slot0, int bs,
+                                          int li, int la) {
   constexpr int NC = Frag<HD>::NC, NT = Frag<HD>::NT;
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
-    f.k[c] = as_bf16x8(ld16(kt + ((int64_t)(la * NC + c) * bs + slot0 + li) * 8));
+  for (int c = 0; c < NC; ++c) {
+    const T* a = kt + ((int64_t)(la * NC + c) * bs + slot0 + li) * 8;
+    f.k[c] = STREAM ? ld16_stream(a) : ld16(a);
+  }
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-    f.v[nt] = *reinterpret_cast<const uint2*>(vt + (int64_t)(16 * nt + li) * bs + slot0 + 4 * la);
+  for (int nt = 0; nt < NT; ++nt) {
+    const T* a = vt + (int64_t)(16 * nt + li) * bs + slot0 + 4 * la;
+    f.v[nt] = STREAM ? ld8_stream(a) : *reinterpret_cast<const uint2*>(a);
+  }
 }
 
 enum { kFull = 0, kTail = 1, kSoft = 2 };
 
+// A row's reference max moves only when a score exceeds it by more than this
+// (log2 units), so probabilities stay below 2^8 between moves.
+constexpr float kRescaleLog2 = 8.0f;
+
+// One 16-token chunk.  limit: tokens of the chunk that are data (kTail);
+// key0, row0, group, k: soft-key causal mask (kSoft).  Cache chunks hold bf16
+// (converted here), the soft chunk fp16.
 template <int HD, int QT, int MODE>
-__device__ __forceinline__ void process_chunk(Frag<HD>& f, const bf16x8 (&qf)[QT][HD / 32],
+__device__ __forceinline__ void process_chunk(Frag<HD>& f, const f16x8 (&qf)[QT][HD / 32],
                                               f32x4 (&o)[QT][HD / 16], float (&m)[QT],
                                               float (&l)[QT], int li, int la, int limit,
                                               int key0, int row0, int group, int k) {
   constexpr int NC = HD / 32, NT = HD / 16;
+  if (MODE != kSoft) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) f.k[c] = bf16x8_to_f16x8(f.k[c]);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) f.v[nt] = bf16x4_to_f16x4(f.v[nt]);
+  }
   if (MODE == kTail) {
     // Tokens at or past `limit` carry arbitrary bytes (NaN poison included):
     // their V entries are replaced by 0 and their scores by -inf.
@@ -79,41 +107,46 @@ __device__ __forceinline__ void process_chunk(Frag<HD>& f, const bf16x8 (&qf)[QT
       f.v[nt].y &= hi;
     }
   }
+  // scores: st[qt][r] is token 4la + r of the chunk, query li of tile qt
+  f32x4 st[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) st[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) st[qt] = mfma16x16x32(as_f16x8(f.k[c]), qf[qt][c], st[qt]);
+  bool move = false;
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    f32x4 st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < NC; ++c) st = mfma16x16x32(f.k[c], qf[qt][c], st);
-    float sc[4] = {st[0], st[1], st[2], st[3]};  // tokens 4la + r, query li
     if (MODE == kTail) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        if (4 * la + r >= limit) sc[r] = -INFINITY;
+        if (4 * la + r >= limit) st[qt][r] = -INFINITY;
     } else if (MODE == kSoft) {
       // soft key j' is visible to query row r iff j' <= r / G (causal, own row included)
       int jmax = (row0 + 16 * qt + li) / group;
       jmax = jmax < k - 1 ? jmax : k - 1;
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        if (key0 + 4 * la + r > jmax) sc[r] = -INFINITY;
+        if (key0 + 4 * la + r > jmax) st[qt][r] = -INFINITY;
     }
-    float cm = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-    cm = fmaxf(cm, __shfl_xor(cm, 16));
-    cm = fmaxf(cm, __shfl_xor(cm, 32));
-    const float mn = fmaxf(m[qt], cm);
-    const float alpha = fast_exp2(m[qt] - mn);
-    bf16x4 pa;
-    float ps = 0.f;
+    const float lmax = fmaxf(fmaxf(st[qt][0], st[qt][1]), fmaxf(st[qt][2], st[qt][3]));
+    move |= lmax > m[qt] + kRescaleLog2;
+  }
+  // Lazy reference max: p = 2^(s - m) with m the row's reference, which only
+  // moves (with the cross-lane reduction and the rescale of l and O) when some
+  // score exceeds it by more than kRescaleLog2.
+  if (__any(move)) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float pv = fast_exp2(sc[r] - mn);
-      ps += pv;
-      pa[r] = (bf16)pv;
-    }
-    l[qt] = l[qt] * alpha + ps;
-    m[qt] = mn;
-    // O rows held by this lane are queries 4la + r; their factors live in lanes 4la + r.
-    if (__any(alpha != 1.0f)) {
+    for (int qt = 0; qt < QT; ++qt) {
+      float lmax = fmaxf(fmaxf(st[qt][0], st[qt][1]), fmaxf(st[qt][2], st[qt][3]));
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+      const float mn = fmaxf(m[qt], lmax);
+      const float alpha = fast_exp2(m[qt] - mn);
+      l[qt] *= alpha;
+      m[qt] = mn;
+      // O rows held by this lane are queries 4la + r; their factors live in lanes 4la + r.
       float ar[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, 4 * la + r);
@@ -122,12 +155,28 @@ __device__ __forceinline__ void process_chunk(Frag<HD>& f, const bf16x8 (&qf)[QT
 #pragma unroll
         for (int r = 0; r < 4; ++r) o[qt][nt][r] *= ar[r];
     }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) o[qt][nt] = mfma16x16x16(pa, f.v[nt], o[qt][nt]);
   }
+  f16x4 pa[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float pv = fast_exp2(st[qt][r] - m[qt]);
+      ps += pv;
+      pa[qt][r] = (f16)pv;
+    }
+    l[qt] += ps;
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int qt = 0; qt < QT; ++qt) o[qt][nt] = mfma16x16x16(pa[qt], as_f16x4(f.v[nt]), o[qt][nt]);
 }
 
-template <int HD, int QT>
+// DEPTH fragment buffers rotate: while chunk i runs, chunks i+1 .. i+DEPTH-1 are
+// in flight.
+template <int HD, int QT, int DEPTH>
 __global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
   constexpr int NC = HD / 32, NT = HD / 16;
   const int lane = threadIdx.x, li = lane & 15, la = lane >> 4;
@@ -142,13 +191,13 @@ __global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
   const int row0 = qg * 16 * QT;
   const int bs = 1 << p.bs_log2;
 
-  const bf16* qb = (const bf16*)p.q + (((int64_t)b * p.n_kv + g) * p.r_alloc + row0) * HD;
-  bf16x8 qf[QT][NC];
+  const f16* qb = (const f16*)p.q + (((int64_t)b * p.n_kv + g) * p.r_alloc + row0) * HD;
+  f16x8 qf[QT][NC];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
     for (int c = 0; c < NC; ++c)
-      qf[qt][c] = as_bf16x8(ld16(qb + (int64_t)(16 * qt + li) * HD + 8 * (la * NC + c)));
+      qf[qt][c] = as_f16x8(ld16(qb + (int64_t)(16 * qt + li) * HD + 8 * (la * NC + c)));
 
   f32x4 o[QT][NT];
   float m[QT], l[QT];
@@ -161,11 +210,11 @@ __global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
   }
 
   if (s == 0) {
-    const bf16* kt = (const bf16*)p.k_soft + ((int64_t)b * p.n_kv + g) * p.ks * HD;
-    const bf16* vt = (const bf16*)p.v_soft + (int64_t)g * HD * p.ks;
+    const f16* kt = (const f16*)p.k_soft + ((int64_t)b * p.n_kv + g) * p.ks * HD;
+    const f16* vt = (const f16*)p.v_soft + (int64_t)g * HD * p.ks;
     for (int c0 = 0; c0 < p.k; c0 += 16) {
       Frag<HD> f;
-      load_frag<HD>(f, kt, vt, c0, p.ks, li, la);
+      load_frag<HD, false>(f, kt, vt, c0, p.ks, li, la);
       process_chunk<HD, QT, kSoft>(f, qf, o, m, l, li, la, 0, c0, row0, p.group, p.k);
     }
   }
@@ -177,26 +226,30 @@ __global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
     // its first token is valid, so the block is one the sequence owns.
     auto load_cache = [&](Frag<HD>& f, int c0) {
       const int64_t blk = phys_block(p, b, c0);
-      load_frag<HD>(f, kbase + blk * p.k_sb, vbase + blk * p.v_sb, c0 & (bs - 1), bs, li, la);
+      load_frag<HD, true>(f, kbase + blk * p.k_sb, vbase + blk * p.v_sb, c0 & (bs - 1), bs, li, la);
     };
-    // Full chunks alternate between two fragment buffers: the loads of the next
-    // chunk are in flight while the current one runs.  Prefetch addresses are
-    // clamped to the last full chunk, so every load stays inside the sequence.
+    // Prefetch addresses are clamped to the last full chunk, so every load
+    // stays inside the sequence.
     const int nfull = (t1 - t0) >> 4, rem = (t1 - t0) & 15;
-    Frag<HD> fa, fb;
-    if (nfull > 0) load_cache(fa, t0);
-    int i = 0;
-    for (; i + 1 < nfull; i += 2) {
-      load_cache(fb, t0 + 16 * (i + 1));
-      process_chunk<HD, QT, kFull>(fa, qf, o, m, l, li, la, 16, 0, row0, p.group, p.k);
-      const int nx = i + 2 < nfull ? i + 2 : nfull - 1;
-      load_cache(fa, t0 + 16 * nx);
-      process_chunk<HD, QT, kFull>(fb, qf, o, m, l, li, la, 16, 0, row0, p.group, p.k);
+    Frag<HD> buf[DEPTH];
+    if (nfull > 0) {
+#pragma unroll
+      for (int j = 0; j < DEPTH - 1; ++j) load_cache(buf[j], t0 + 16 * (j < nfull ? j : nfull - 1));
     }
-    if (i < nfull) process_chunk<HD, QT, kFull>(fa, qf, o, m, l, li, la, 16, 0, row0, p.group, p.k);
+    for (int i = 0; i < nfull; i += DEPTH) {
+#pragma unroll
+      for (int u = 0; u < DEPTH; ++u) {
+        if (i + u < nfull) {
+          const int nx = i + u + DEPTH - 1;
+          load_cache(buf[(u + DEPTH - 1) % DEPTH], t0 + 16 * (nx < nfull ? nx : nfull - 1));
+          process_chunk<HD, QT, kFull>(buf[u], qf, o, m, l, li, la, 16, 0, row0, p.group, p.k);
+        }
+      }
+    }
     if (rem) {
-      load_cache(fb, t0 + 16 * nfull);
-      process_chunk<HD, QT, kTail>(fb, qf, o, m, l, li, la, rem, 0, row0, p.group, p.k);
+      Frag<HD> f;
+      load_cache(f, t0 + 16 * nfull);
+      process_chunk<HD, QT, kTail>(f, qf, o, m, l, li, la, rem, 0, row0, p.group, p.k);
     }
   }
 
@@ -362,12 +415,15 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
 
 }  // namespace
 
+// Prefetch depth of the production instantiation.
+constexpr int kAttnDepth = SP_ATTN_DEPTH;
+
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int qt, int batch, hipStream_t s) {
   const dim3 grid(p.max_splits, p.n_kv * p.n_qgroups, batch);
-#define SP_ATTN_CASE(HD_, QT_)                                              \
-  if (hd == HD_ && qt == QT_) {                                             \
-    hipLaunchKernelGGL((attn_split_bf16<HD_, QT_>), grid, dim3(64), 0, s, p); \
-    return hipGetLastError();                                               \
+#define SP_ATTN_CASE(HD_, QT_)                                                                  \
+  if (hd == HD_ && qt == QT_) {                                                                 \
+    hipLaunchKernelGGL((attn_split_bf16<HD_, QT_, kAttnDepth>), grid, dim3(64), 0, s, p);  \
+    return hipGetLastError();                                                                   \
   }
   SP_ATTN_CASE(128, 1) SP_ATTN_CASE(128, 2) SP_ATTN_CASE(128, 3) SP_ATTN_CASE(128, 4)
   SP_ATTN_CASE(64, 1) SP_ATTN_CASE(64, 2) SP_ATTN_CASE(64, 3) SP_ATTN_CASE(64, 4)
@@ -389,8 +445,8 @@ hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStrea
 
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s) {
   const dim3 grid((p.rows + 3) / 4, p.n_kv, batch);
-  if (dt == kBF16)
-    hipLaunchKernelGGL(merge_splits<bf16>, grid, dim3(256), 0, s, p);
+  if (dt == kBF16)  // the attention output feeds an fp16 MFMA
+    hipLaunchKernelGGL(merge_splits<f16>, grid, dim3(256), 0, s, p);
   else
     hipLaunchKernelGGL(merge_splits<float>, grid, dim3(256), 0, s, p);
   return hipGetLastError();

@@ -1,10 +1,12 @@
 // Projections of the probe's decoder layer: C = A W^T with A [M][K] and the
 // weight W [N][K] both K-contiguous, fused epilogues (residual adds, SwiGLU).
 //
-// bf16 path: v_mfma_f32_16x16x32_bf16, 256 threads as 2 x 2 waves, a
-// BM x BN x 64 tile staged in LDS (rows padded by 16 bytes so the 16 lanes of
-// an MFMA fragment read hit distinct banks), two LDS buffers: the next K-step
-// is fetched into registers while the current one runs on the matrix cores.
+// bf16 path: fp16 activations A, bf16 weights converted exactly to fp16 while
+// they are staged into LDS (|w| in [2^-14, 65504]), v_mfma_f32_16x16x32_f16 with
+// fp32 accumulation.  256 threads as 2 x 2 waves, a BM x BN x 64 tile staged in
+// LDS (rows padded by 16 bytes so the 16 lanes of an MFMA fragment read hit
+// distinct banks), two LDS buffers: the next K-step is fetched into registers
+// while the current one runs on the matrix cores.
 // SwiGLU: the BN weight rows of a tile alternate 16 gate rows and the 16
 // matching up rows, so every lane holds gate and up of the same outputs.
 #include "common.h"
@@ -30,20 +32,20 @@ __device__ __forceinline__ const bf16* weight_row(const GemmParams& p, int tile_
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
 template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(256) void gemm_bf16(const GemmParams p) {
+__global__ __launch_bounds__(256) void gemm_mfma(const GemmParams p) {
   constexpr int BK = 64, LD = BK + 8;
   constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
   constexpr int AU = BM * 8 / 256, BU = BN * 8 / 256;  // 16-byte chunks per thread
   static_assert(AU >= 1 && BU >= 1, "tile too small");
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LD];
+  __shared__ __attribute__((aligned(16))) f16 As[2][BM * LD];
+  __shared__ __attribute__((aligned(16))) f16 Bs[2][BN * LD];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, li = lane & 15, la = lane >> 4;
   const int n_blk = blockIdx.x, m0 = blockIdx.y * BM, n0 = n_blk * BN;
-  const bf16* A = (const bf16*)p.a;
+  const f16* A = (const f16*)p.a;
 
-  const bf16* arow[AU];
+  const f16* arow[AU];
   const bf16* brow[BU];
   int aoff[AU], boff[BU];
 #pragma unroll
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(256) void gemm_bf16(const GemmParams p) {
 #pragma unroll
     for (int u = 0; u < AU; ++u) ra[u] = ld16(arow[u] + k0);
 #pragma unroll
-    for (int u = 0; u < BU; ++u) rb[u] = ld16(brow[u] + k0);
+    for (int u = 0; u < BU; ++u) rb[u] = bf16x8_to_f16x8(ld16(brow[u] + k0));
   };
   auto lstore = [&](int buf) {
 #pragma unroll
@@ -90,13 +92,13 @@ __global__ __launch_bounds__(256) void gemm_bf16(const GemmParams p) {
     if (kt + 1 < KT) gload(kt + 1);
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 af[MT], bfr[NT];
+      f16x8 af[MT], bfr[NT];
 #pragma unroll
       for (int i = 0; i < MT; ++i)
-        af[i] = as_bf16x8(ld16(&As[buf][(wm * WM + 16 * i + li) * LD + kk * 32 + 8 * la]));
+        af[i] = as_f16x8(ld16(&As[buf][(wm * WM + 16 * i + li) * LD + kk * 32 + 8 * la]));
 #pragma unroll
       for (int j = 0; j < NT; ++j)
-        bfr[j] = as_bf16x8(ld16(&Bs[buf][(wn * WN + 16 * j + li) * LD + kk * 32 + 8 * la]));
+        bfr[j] = as_f16x8(ld16(&Bs[buf][(wn * WN + 16 * j + li) * LD + kk * 32 + 8 * la]));
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -119,7 +121,7 @@ __global__ __launch_bounds__(256) void gemm_bf16(const GemmParams p) {
           const int pair = (wn * WN + 16 * j) >> 5;
           const int n = n_blk * (BN / 2) + 16 * pair + li;
           const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-          ((bf16*)p.c)[(int64_t)m * p.ldc + n] = (bf16)(silu(gt) * up);
+          ((f16*)p.c)[(int64_t)m * p.ldc + n] = (f16)(silu(gt) * up);
         }
       } else {
 #pragma unroll
@@ -170,13 +172,13 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
 }
 
 template <int BM, int BN>
-hipError_t launch_bf16_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
+hipError_t launch_mfma_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
   const dim3 grid(p.N / BN, (p.M + BM - 1) / BM);
   switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_bf16<BM, BN, kEpiStore>), grid, dim3(256), 0, s, p); break;
-    case kEpiResidRow: hipLaunchKernelGGL((gemm_bf16<BM, BN, kEpiResidRow>), grid, dim3(256), 0, s, p); break;
-    case kEpiResidF32: hipLaunchKernelGGL((gemm_bf16<BM, BN, kEpiResidF32>), grid, dim3(256), 0, s, p); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_bf16<BM, BN, kEpiSwiglu>), grid, dim3(256), 0, s, p); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiStore>), grid, dim3(256), 0, s, p); break;
+    case kEpiResidRow: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiResidRow>), grid, dim3(256), 0, s, p); break;
+    case kEpiResidF32: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiResidF32>), grid, dim3(256), 0, s, p); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiSwiglu>), grid, dim3(256), 0, s, p); break;
   }
   return hipGetLastError();
 }
@@ -216,10 +218,10 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
   switch (best) {
-    case 0: return launch_bf16_tile<128, 128>(epi, p, s);
-    case 1: return launch_bf16_tile<64, 128>(epi, p, s);
-    case 2: return launch_bf16_tile<32, 128>(epi, p, s);
-    case 3: return launch_bf16_tile<32, 64>(epi, p, s);
+    case 0: return launch_mfma_tile<128, 128>(epi, p, s);
+    case 1: return launch_mfma_tile<64, 128>(epi, p, s);
+    case 2: return launch_mfma_tile<32, 128>(epi, p, s);
+    case 3: return launch_mfma_tile<32, 64>(epi, p, s);
   }
   return hipErrorInvalidValue;
 }

@@ -6,7 +6,8 @@
 
 namespace sp {
 
-enum DType { kF32 = 0, kBF16 = 1 };
+// Storage types; bf16-storage configs compute with fp16 activations (kF16).
+enum DType { kF32 = 0, kBF16 = 1, kF16 = 2 };
 
 // ---------------------------------------------------------------- soft-row prep
 // out[r][i] = x[r][i] / sqrt(mean_i x[r][i]^2 + eps) * gain[i], rows r < rows.
@@ -18,13 +19,14 @@ struct RopeParams {
   const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32
   const int* seq_lens;     // device [B]
   const int* err;          // nullable: skip everything if *err != 0
-  void* q;                 // [B][n_kv][r_alloc][hd]           (compute dtype), scaled
+  void* q;                 // [B][n_kv][r_alloc][hd]           (activation dtype), scaled
   void* k_soft;            // [B][n_kv] tiles of ks tokens, chunked layout (x = 16 B / elem)
   void* v_soft;            // [n_kv][hd][ks] (batch-invariant)
   int n_q, n_kv, hd, k, group, r_alloc, ks, max_seq_len;
   double rope_base;
   float q_scale;           // log2(e) / sqrt(hd)
 };
+// dt: activation dtype of the outputs (kF32 or kF16)
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
@@ -53,20 +55,21 @@ struct MergeParams {
   const float2* ml_part;
   const int* seq_lens;
   const int* err;
-  void* out;               // [B k][n_q hd] (compute dtype)
+  void* out;               // [B k][n_q hd] (activation dtype)
   int n_kv, group, k, rows, r_alloc, hd, max_splits, split_len, max_seq_len, n_q;
 };
+// dt: storage dtype of the config (the output is fp16 for bf16 storage)
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s);
 
 // ---------------------------------------------------------------- GEMM
 enum Epilogue {
   kEpiStore = 0,      // C fp32 = acc
-  kEpiResidRow = 1,   // C fp32 = acc + R[m % r_mod][n]   (R in the compute dtype)
+  kEpiResidRow = 1,   // C fp32 = acc + R[m % r_mod][n]   (R in the storage dtype)
   kEpiResidF32 = 2,   // C fp32 = acc + R[m][n]           (R fp32, ld = ldc)
-  kEpiSwiglu = 3      // C (compute dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
+  kEpiSwiglu = 3      // C (activation dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
 };
 struct GemmParams {
-  const void* a;           // [M][lda]
+  const void* a;           // [M][lda], activation dtype (fp16 for bf16 storage)
   const void* b[3];        // weight row blocks: rows [0, b_split0) from b[0], [b_split0, b_split1)
                            // from b[1], the rest from b[2]; SwiGLU: b[0] gate, b[1] up
   int b_split0, b_split1;
@@ -75,6 +78,7 @@ struct GemmParams {
   const void* r;           // residual
   int M, N, K, lda, ldc, r_mod;
 };
+// dt: storage dtype of the weights (kF32: fp32 VALU path; kBF16: fp16 MFMA path)
 hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s);
 
 // ---------------------------------------------------------------- read-out

@@ -122,10 +122,10 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
                                hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   const dim3 grid(rows), block(256);
-  if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kBF16)
-    hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, bf16>), grid, block, 0, s, (const bf16*)x, (const bf16*)gain, (bf16*)out, d, eps);
-  else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kBF16)
-    hipLaunchKernelGGL((rmsnorm_rows<float, bf16, bf16>), grid, block, 0, s, (const float*)x, (const bf16*)gain, (bf16*)out, d, eps);
+  if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
+    hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, (const bf16*)gain, (f16*)out, d, eps);
+  else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kF16)
+    hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16>), grid, block, 0, s, (const float*)x, (const bf16*)gain, (f16*)out, d, eps);
   else if (in_dt == kF32 && gain_dt == kF32 && out_dt == kF32)
     hipLaunchKernelGGL((rmsnorm_rows<float, float, float>), grid, block, 0, s, (const float*)x, (const float*)gain, (float*)out, d, eps);
   else
@@ -135,10 +135,12 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
 
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.k, p.n_q + 2 * p.n_kv, batch), block(p.hd / 2);
-  if (dt == kBF16)
-    hipLaunchKernelGGL(rope_scatter<bf16>, grid, block, 0, s, p);
-  else
+  if (dt == kF16)
+    hipLaunchKernelGGL(rope_scatter<f16>, grid, block, 0, s, p);
+  else if (dt == kF32)
     hipLaunchKernelGGL(rope_scatter<float>, grid, block, 0, s, p);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -75,9 +75,9 @@ Plan make_plan(const sp_probe_config& c) {
   if (c.split_len) {
     p.split_len = c.split_len;
   } else {
-    // at most 16 splits per sequence, between 1024 and 8192 tokens each
+    // at most 8 splits per sequence, between 1024 and 16384 tokens each
     int sl = 1024;
-    while (sl < 8192 && (int64_t)sl * 16 < c.max_seq_len) sl *= 2;
+    while (sl < 16384 && (int64_t)sl * 8 < c.max_seq_len) sl *= 2;
     p.split_len = sl;
   }
   p.max_splits = c.max_seq_len > 0 ? (c.max_seq_len + p.split_len - 1) / p.split_len : 1;
@@ -240,7 +240,8 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   if (!block_table && (int64_t)B * kv->max_blocks_per_seq > kv->num_blocks) return SP_ERR_INVALID_ARG;
 
   hipStream_t s = (hipStream_t)stream;
-  const DType dt = c.dtype == SP_BF16 ? kBF16 : kF32;
+  const DType dt = c.dtype == SP_BF16 ? kBF16 : kF32;   // storage: weights, soft prompt, KV
+  const DType at_dt = c.dtype == SP_BF16 ? kF16 : kF32;  // activations feeding the MFMAs
   const int d = c.hidden, hd = c.head_dim, I = c.intermediate, M = B * c.k;
   const bool debug = c.flags & SP_FLAG_DEBUG;
   const bool prof = c.flags & SP_FLAG_PROFILE;
@@ -260,7 +261,7 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   if (!mark()) return SP_ERR_HIP;
 
   // stage 0: soft rows — RMSNorm, Q/K/V on the k distinct rows, RoPE per sequence
-  SP_TRY(launch_rmsnorm_rows(dt, dt, dt, soft_prompt, wt->in_norm, at<void>(h, pl.off_u), c.k, d,
+  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, wt->in_norm, at<void>(h, pl.off_u), c.k, d,
                              c.rms_eps, s));
   {
     GemmParams g{};
@@ -285,7 +286,7 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     r.r_alloc = pl.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
     r.rope_base = c.rope_base;
     r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
-    SP_TRY(launch_rope_scatter(dt, r, B, s));
+    SP_TRY(launch_rope_scatter(at_dt, r, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
@@ -339,7 +340,7 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   if (!mark()) return SP_ERR_HIP;
 
   // stage 4: w = RMSNorm(a; gamma_post)
-  SP_TRY(launch_rmsnorm_rows(kF32, dt, dt, at<void>(h, pl.off_a), wt->post_norm,
+  SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, at<void>(h, pl.off_a), wt->post_norm,
                              at<void>(h, pl.off_w), M, d, c.rms_eps, s));
   if (!mark()) return SP_ERR_HIP;
 

@@ -62,10 +62,10 @@ def test_small_taps_match_oracle(w, dev):
     probe = binding.Probe(w)
     probe.forward(kv_d, p_d)
     B, k, d = w.batch, w.k, w.hidden
-    dt = inputs.TORCH_DTYPE[w.dtype]
+    act = torch.float16 if w.dtype == "bf16" else torch.float32  # activations feeding the MFMAs
     outs = H.oracle_outputs(w, kv, params, range(B))
     qkv = probe.tap(binding.SP_TAP_QKV, B, dev).view(torch.float32).cpu().double().numpy()
-    attn = probe.tap(binding.SP_TAP_ATTN, B, dev).view(dt).cpu().double().numpy()
+    attn = probe.tap(binding.SP_TAP_ATTN, B, dev).view(act).cpu().double().numpy()
     a = probe.tap(binding.SP_TAP_A, B, dev).view(torch.float32).cpu().double().numpy()
     y = probe.tap(binding.SP_TAP_Y, B, dev).view(torch.float32).cpu().double().numpy()
     probe.close()
@@ -73,8 +73,9 @@ def test_small_taps_match_oracle(w, dev):
     from oracle import probe as oracle
     u = oracle.rms_norm(params["soft_prompt"].double().numpy(), W["in_norm"], w.rms_eps)
     qkv_ref = np.concatenate([u @ W["w_q"].T, u @ W["w_k"].T, u @ W["w_v"].T], axis=1)
-    # relative to the magnitude of each tensor: fp32 path ~1e-6, bf16 path ~1e-2
-    rel = 1e-4 if w.dtype == "f32" else 3e-2
+    # relative to the magnitude of each tensor: fp32 path ~1e-6; bf16-storage path
+    # (fp16 operands, a few roundings of 2^-11) ~1e-3
+    rel = 1e-4 if w.dtype == "f32" else 1e-2
 
     def close(x, r, what):
         scale = max(np.max(np.abs(r)), 1e-30)
