@@ -10,28 +10,27 @@
 // partial; the merge combines partials with the log-sum-exp rule
 //   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  O = sum_s O_s 2^(m_s - M) / L.
 //
-// bf16 path (bf16 KV cache, fp16 MFMA operands, fp32 accumulation), per
-// 16-token chunk (always inside one block, so one block-table lookup per chunk,
-// uniform across the wave):
-//   S^T = K Q^T on v_mfma_f32_16x16x32_f16 with the 16 tokens as MFMA rows:
-//   lane (li, la) loads K row li (16-byte pieces of the chunked K tile) and,
-//   after the MFMA, holds the scores of tokens 4la .. 4la+3 for query li.  That
-//   is exactly the A operand of v_mfma_f32_16x16x16_f16 (query row li, 4
-//   consecutive tokens), so P never goes through LDS.
-//   O += P V with V as the B operand: lane (li, la) needs V[4la .. 4la+3][16nt + li],
-//   one 8-byte load from the dim-major V tile; the 16 lanes of a row read 512
-//   contiguous bytes.  K and V are loaded as bf16 with streaming loads and
-//   converted to fp16 in registers (exact for |x| in [2^-14, 65504]); the queries
-//   and the soft rows' K/V arrive in fp16.
-//   All query tiles' QK products are issued before any softmax work, and one
-//   wave-wide test per chunk decides whether a reference max must move, so the
-//   common path is one basic block the scheduler can overlap.
+// bf16 path: bf16 KV cache, bf16 MFMA operands, fp32 accumulation.  The two
+// operands the kernel itself rounds, the queries and the probabilities, are
+// carried as hi + lo bf16 pairs (x = hi + lo to ~16 bits), so every product
+// is K*Q_hi + K*Q_lo and P_hi*V + P_lo*V with K and V exact as stored.
+// One workgroup per (sequence, KV head, query group, split) with one wave per
+// 16-row query tile.  The split's tokens are consumed in units of 32 (two
+// 16-token halves, each inside one block):
+//   * all lanes of the workgroup fetch the unit's K and V tiles with 16-byte
+//     streaming loads (1 KB contiguous per wave instruction), two units ahead,
+//     and copy them into one of two LDS stages (in a tail unit, slots past the
+//     end are zeroed on the way: their bytes may be anything, NaN included);
+//   * every wave reads its fragments from LDS and runs its query tile:
+//     S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with a half's 16 tokens as MFMA
+//     rows, so lane (li, la) ends up with tokens 4la..4la+3 of both halves for
+//     query li: 8 values = the A operand of v_mfma_f32_16x16x32_bf16 for
+//     O += P V (k-slot 4h + r stands for token 16h + 4la + r); P never goes
+//     through LDS; the B operand is V[those 8 tokens][16nt + li], which the
+//     staging has placed in 16 contiguous bytes (one conflict-free LDS read).
+// Online softmax in log2 units with a lazy reference max (see kRescaleLog2).
 #include "common.h"
 #include "kernels.h"
-
-#ifndef SP_ATTN_DEPTH
-#define SP_ATTN_DEPTH 3
-#endif
 
 namespace sp {
 namespace {
@@ -47,139 +46,195 @@ __device__ __forceinline__ int64_t phys_block(const AttnParams& p, int b, int t)
                        : (int64_t)b * p.mbps + lb;
 }
 
-template <int HD>
-struct Frag {
-  static constexpr int NC = HD / 32;  // 32-wide head-dim chunks (QK contraction)
-  static constexpr int NT = HD / 16;  // 16-wide head-dim tiles (PV output)
-  uint4 k[NC];                        // K[token li][8 (la*NC + c) .. +7]
-  uint2 v[NT];                        // V[tokens 4la .. 4la+3][16nt + li]
-};
-
-// kt/vt: K and V tile bases of the block holding the chunk, slot0: slot of the
-// chunk's first token in that block, bs: tile length in tokens.  STREAM: the
-// KV cache, read once (non-temporal loads).
-template <int HD, bool STREAM, typename T>
-__device__ __forceinline__ void load_frag(Frag<HD>& f, const T* kt, const T* vt, int slot0, int bs,
-                                          int li, int la) {
-  constexpr int NC = Frag<HD>::NC, NT = Frag<HD>::NT;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const T* a = kt + ((int64_t)(la * NC + c) * bs + slot0 + li) * 8;
-    f.k[c] = STREAM ? ld16_stream(a) : ld16(a);
-  }
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const T* a = vt + (int64_t)(16 * nt + li) * bs + slot0 + 4 * la;
-    f.v[nt] = STREAM ? ld8_stream(a) : *reinterpret_cast<const uint2*>(a);
-  }
-}
-
-enum { kFull = 0, kTail = 1, kSoft = 2 };
-
 // A row's reference max moves only when a score exceeds it by more than this
 // (log2 units), so probabilities stay below 2^8 between moves.
 constexpr float kRescaleLog2 = 8.0f;
 
-// One 16-token chunk.  limit: tokens of the chunk that are data (kTail);
-// key0, row0, group, k: soft-key causal mask (kSoft).  Cache chunks hold bf16
-// (converted here), the soft chunk fp16.
-template <int HD, int QT, int MODE>
-__device__ __forceinline__ void process_chunk(Frag<HD>& f, const f16x8 (&qf)[QT][HD / 32],
-                                              f32x4 (&o)[QT][HD / 16], float (&m)[QT],
-                                              float (&l)[QT], int li, int la, int limit,
-                                              int key0, int row0, int group, int k) {
+// The wave's running softmax state for its 16 query rows.
+template <int HD>
+struct RowState {
+  static constexpr int NC = HD / 32, NT = HD / 16;
+  bf16x8 qh[NC], ql[NC];  // Q[row li][8 (la*NC + c) .. +7], hi and lo parts
+  f32x4 o[NT];            // O[row 4la + r][16nt + li], unnormalised
+  float m, l;             // reference max of row li (log2 units); this lane's part of its sum
+};
+
+// One 32-token unit for one wave.  kf[h][c]: K[token li of half h][8 (la*NC + c) ..];
+// vf[nt]: V[tokens 4la..4la+3 of half 0, then of half 1][16nt + li].  SOFT: the soft keys,
+// whose K and V are themselves hi + lo pairs (kl, vl) and whose visibility is
+// causal; cache units mask keys at or past `limit`.
+template <int HD, bool SOFT>
+__device__ __forceinline__ void run_unit(RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
+                                         const bf16x8 (&vf)[HD / 16],
+                                         const bf16x8 (&kl)[2][HD / 32],
+                                         const bf16x8 (&vl)[HD / 16], int li, int la,
+                                         int limit, int key0, int row, int group, int k) {
   constexpr int NC = HD / 32, NT = HD / 16;
-  if (MODE != kSoft) {
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int c = 0; c < NC; ++c) f.k[c] = bf16x8_to_f16x8(f.k[c]);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) f.v[nt] = bf16x4_to_f16x4(f.v[nt]);
-  }
-  if (MODE == kTail) {
-    // Tokens at or past `limit` carry arbitrary bytes (NaN poison included):
-    // their V entries are replaced by 0 and their scores by -inf.
-    const int keep = limit - 4 * la;  // tokens of this lane kept: 4la + r < limit
-    const uint32_t lo = keep >= 2 ? 0xffffffffu : (keep == 1 ? 0x0000ffffu : 0u);
-    const uint32_t hi = keep >= 4 ? 0xffffffffu : (keep == 3 ? 0x0000ffffu : 0u);
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      f.v[nt].x &= lo;
-      f.v[nt].y &= hi;
+  for (int c = 0; c < NC; ++c) {
+    s0 = mfma16x16x32_bf16(kf[0][c], st.qh[c], s0);
+    s1 = mfma16x16x32_bf16(kf[1][c], st.qh[c], s1);
+    s0 = mfma16x16x32_bf16(kf[0][c], st.ql[c], s0);
+    s1 = mfma16x16x32_bf16(kf[1][c], st.ql[c], s1);
+    if (SOFT) {
+      s0 = mfma16x16x32_bf16(kl[0][c], st.qh[c], s0);
+      s1 = mfma16x16x32_bf16(kl[1][c], st.qh[c], s1);
     }
   }
-  // scores: st[qt][r] is token 4la + r of the chunk, query li of tile qt
-  f32x4 st[QT];
+  float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+  if (SOFT) {
+    // soft key j' is visible to query row r iff j' <= r / G (causal, own row included)
+    int jmax = row / group;
+    jmax = jmax < k - 1 ? jmax : k - 1;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) st[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < 8; ++i)
+      if (key0 + 16 * (i >> 2) + 4 * la + (i & 3) > jmax) sc[i] = -INFINITY;
+  } else if (limit < 32) {
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) st[qt] = mfma16x16x32(as_f16x8(f.k[c]), qf[qt][c], st[qt]);
-  bool move = false;
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    if (MODE == kTail) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (4 * la + r >= limit) st[qt][r] = -INFINITY;
-    } else if (MODE == kSoft) {
-      // soft key j' is visible to query row r iff j' <= r / G (causal, own row included)
-      int jmax = (row0 + 16 * qt + li) / group;
-      jmax = jmax < k - 1 ? jmax : k - 1;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (key0 + 4 * la + r > jmax) st[qt][r] = -INFINITY;
-    }
-    const float lmax = fmaxf(fmaxf(st[qt][0], st[qt][1]), fmaxf(st[qt][2], st[qt][3]));
-    move |= lmax > m[qt] + kRescaleLog2;
+    for (int i = 0; i < 8; ++i)
+      if (16 * (i >> 2) + 4 * la + (i & 3) >= limit) sc[i] = -INFINITY;
   }
+  float lmax = sc[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) lmax = fmaxf(lmax, sc[i]);
   // Lazy reference max: p = 2^(s - m) with m the row's reference, which only
   // moves (with the cross-lane reduction and the rescale of l and O) when some
   // score exceeds it by more than kRescaleLog2.
-  if (__any(move)) {
+  if (__any(lmax > st.m + kRescaleLog2)) {
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
+    const float mn = fmaxf(st.m, lmax);
+    const float alpha = fast_exp2(st.m - mn);
+    st.l *= alpha;
+    st.m = mn;
+    // O rows held by this lane are queries 4la + r; their factors live in lanes 4la + r.
+    float ar[4];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      float lmax = fmaxf(fmaxf(st[qt][0], st[qt][1]), fmaxf(st[qt][2], st[qt][3]));
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-      lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
-      const float mn = fmaxf(m[qt], lmax);
-      const float alpha = fast_exp2(m[qt] - mn);
-      l[qt] *= alpha;
-      m[qt] = mn;
-      // O rows held by this lane are queries 4la + r; their factors live in lanes 4la + r.
-      float ar[4];
+    for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, 4 * la + r);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ar[r] = __shfl(alpha, 4 * la + r);
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) o[qt][nt][r] *= ar[r];
-    }
+      for (int r = 0; r < 4; ++r) st.o[nt][r] *= ar[r];
   }
-  f16x4 pa[QT];
+  bf16x8 ph, pl;
+  float ps = 0.f;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    float ps = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float pv = fast_exp2(st[qt][r] - m[qt]);
-      ps += pv;
-      pa[qt][r] = (f16)pv;
-    }
-    l[qt] += ps;
+  for (int i = 0; i < 8; ++i) {
+    const float pv = fast_exp2(sc[i] - st.m);
+    ps += pv;
+    ph[i] = (bf16)pv;
+    pl[i] = (bf16)(pv - (float)ph[i]);
   }
+  st.l += ps;
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt) o[qt][nt] = mfma16x16x16(pa[qt], as_f16x4(f.v[nt]), o[qt][nt]);
+  for (int nt = 0; nt < NT; ++nt) {
+    st.o[nt] = mfma16x16x32_bf16(ph, vf[nt], st.o[nt]);
+    st.o[nt] = mfma16x16x32_bf16(pl, vf[nt], st.o[nt]);
+    if (SOFT) st.o[nt] = mfma16x16x32_bf16(ph, vl[nt], st.o[nt]);
+  }
 }
 
-// DEPTH fragment buffers rotate: while chunk i runs, chunks i+1 .. i+DEPTH-1 are
-// in flight.
-template <int HD, int QT, int DEPTH>
-__global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
+// Pieces of a 32-token unit, as fetched: 16 bytes each; for half h (16 tokens),
+// KP pieces of the K tile (piece c8*16 + t: head dims 8 c8 .. 8 c8 + 7 of
+// token t) followed by KP pieces of the V tile (piece 2 i + e: tokens
+// 8e .. 8e + 7 of head dim i).
+// LDS stage layout: K as fetched, [h][c8][t] in 16-byte pieces (index
+// h*KP + c8*16 + t); then V in 8-byte quads of 4 tokens, ordered
+// [nt][la][li][h] with head dim i = 16 nt + li and tokens 4 la .. 4 la + 3 of
+// half h, so the PV operand of lane (li, la) -- tokens 4la..4la+3 of both
+// halves -- is 16 contiguous bytes and a wave's read is 1 KB contiguous.
+template <int HD, int W>
+struct Unit {
+  static constexpr int KP = 2 * HD;                       // pieces per half per tensor
+  static constexpr int NP = 4 * KP;                       // pieces per unit
+  static constexpr int PPL = (NP + 64 * W - 1) / (64 * W);  // pieces per lane
+  static constexpr bool EXACT = NP % (64 * W) == 0;       // every lane has PPL pieces
+  u32x4 r[PPL];
+};
+
+// Issue the unit's loads.  blk0/blk1, slot0/slot1: block and first slot of each half.
+template <int HD, int W>
+__device__ __forceinline__ void fetch_unit(Unit<HD, W>& un, const bf16* kbase, const bf16* vbase,
+                                           int64_t k_sb, int64_t v_sb, int64_t blk0, int64_t blk1,
+                                           int slot0, int slot1, int bs, int tid) {
+  using U = Unit<HD, W>;
+#pragma unroll
+  for (int j = 0; j < U::PPL; ++j) {
+    const int pc = tid + j * 64 * W;
+    if (U::EXACT || pc < U::NP) {
+      const int h = pc >= 2 * U::KP;
+      const int q = pc - h * 2 * U::KP;
+      const int64_t blk = h ? blk1 : blk0;
+      const int slot = h ? slot1 : slot0;
+      const bf16* a = q < U::KP
+          ? kbase + blk * k_sb + ((int64_t)(q >> 4) * bs + slot + (q & 15)) * 8
+          : vbase + blk * v_sb + (int64_t)((q - U::KP) >> 1) * bs + slot + 8 * ((q - U::KP) & 1);
+      un.r[j] = ld16v_stream(a);
+    }
+  }
+}
+
+// Write the fetched unit into an LDS stage (layout above).  TAIL: slots at or
+// past `limit` are zeroed (their bytes may be anything, NaN included).
+template <int HD, int W, bool TAIL>
+__device__ __forceinline__ void stage_unit(const Unit<HD, W>& un, u32x4* dst, int limit, int tid) {
+  using U = Unit<HD, W>;
+  u32x2* vdst = reinterpret_cast<u32x2*>(dst + 2 * U::KP);
+#pragma unroll
+  for (int j = 0; j < U::PPL; ++j) {
+    const int pc = tid + j * 64 * W;
+    if (U::EXACT || pc < U::NP) {
+      u32x4 v = un.r[j];
+      const int h = pc >= 2 * U::KP;
+      const int q = pc - h * 2 * U::KP;
+      if (q < U::KP) {
+        if (TAIL && 16 * h + (q & 15) >= limit) v = u32x4{0u, 0u, 0u, 0u};
+        dst[h * U::KP + q] = v;
+      } else {
+        const int i = (q - U::KP) >> 1, e = (q - U::KP) & 1;
+        if (TAIL) {
+          const int tk0 = 16 * h + 8 * e;  // first of the piece's 8 tokens
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const int keep = limit - (tk0 + 2 * w);
+            v[w] &= keep >= 2 ? 0xffffffffu : (keep == 1 ? 0x0000ffffu : 0u);
+          }
+        }
+        const int nt = i >> 4, li = i & 15;
+        vdst[((nt * 4 + 2 * e) * 16 + li) * 2 + h] = u32x2{v.x, v.y};      // tokens 8e .. 8e + 3
+        vdst[((nt * 4 + 2 * e + 1) * 16 + li) * 2 + h] = u32x2{v.z, v.w};  // tokens 8e + 4 .. 8e + 7
+      }
+    }
+  }
+}
+
+// A wave's fragments of a staged unit, then the unit's softmax and products.
+template <int HD, int W>
+__device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, int limit, int li,
+                                             int la, int row) {
+  constexpr int NC = HD / 32, NT = HD / 16, KP = Unit<HD, W>::KP;
+  bf16x8 kf[2][NC], vf[NT];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      kf[h][c] = __builtin_bit_cast(bf16x8, sb[h * KP + (la * NC + c) * 16 + li]);
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+    vf[nt] = __builtin_bit_cast(bf16x8, sb[2 * KP + (nt * 4 + la) * 16 + li]);
+  run_unit<HD, false>(st, kf, vf, kf, vf, li, la, limit, 0, row, 1, 1);
+}
+
+// W waves per workgroup, one per 16-row query tile.
+template <int HD, int W>
+__global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   constexpr int NC = HD / 32, NT = HD / 16;
-  const int lane = threadIdx.x, li = lane & 15, la = lane >> 4;
+  using U = Unit<HD, W>;
+  __shared__ u32x4 stage[2][U::NP];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, la = lane >> 4;
+  __builtin_assume(tid < 64 * W);
   const int s = blockIdx.x;
   const int g = blockIdx.y / p.n_qgroups, qg = blockIdx.y % p.n_qgroups;
   const int b = blockIdx.z;
@@ -188,84 +243,100 @@ __global__ __launch_bounds__(64) void attn_split_bf16(const AttnParams p) {
   const int t0 = s * p.split_len;
   if (s > 0 && t0 >= n) return;
   const int t1 = min(n, t0 + p.split_len);
-  const int row0 = qg * 16 * QT;
+  const int row0 = (qg * W + wave) * 16;     // first of this wave's rows in the KV head
   const int bs = 1 << p.bs_log2;
 
-  const f16* qb = (const f16*)p.q + (((int64_t)b * p.n_kv + g) * p.r_alloc + row0) * HD;
-  f16x8 qf[QT][NC];
+  RowState<HD> st;
+  {
+    const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + row0 + li) * HD;
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
+    for (int c = 0; c < NC; ++c) {
+      st.qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qo + 8 * (la * NC + c)));
+      st.ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qo + 8 * (la * NC + c)));
+    }
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      qf[qt][c] = as_f16x8(ld16(qb + (int64_t)(16 * qt + li) * HD + 8 * (la * NC + c)));
-
-  f32x4 o[QT][NT];
-  float m[QT], l[QT];
-#pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    m[qt] = kNegBig;
-    l[qt] = 0.f;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) o[qt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nt = 0; nt < NT; ++nt) st.o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st.m = kNegBig;
+    st.l = 0.f;
   }
 
   if (s == 0) {
-    const f16* kt = (const f16*)p.k_soft + ((int64_t)b * p.n_kv + g) * p.ks * HD;
-    const f16* vt = (const f16*)p.v_soft + (int64_t)g * HD * p.ks;
-    for (int c0 = 0; c0 < p.k; c0 += 16) {
-      Frag<HD> f;
-      load_frag<HD, false>(f, kt, vt, c0, p.ks, li, la);
-      process_chunk<HD, QT, kSoft>(f, qf, o, m, l, li, la, 0, c0, row0, p.group, p.k);
+    // the soft keys: hi/lo bf16 tiles of ks tokens (a multiple of 32), read in place
+    const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * HD, vo = (int64_t)g * HD * p.ks;
+    const bf16 *kt = (const bf16*)p.k_soft + ko, *ktl = (const bf16*)p.k_soft_lo + ko;
+    const bf16 *vt = (const bf16*)p.v_soft + vo, *vtl = (const bf16*)p.v_soft_lo + vo;
+    for (int c0 = 0; c0 < p.k; c0 += 32) {
+      bf16x8 kf[2][NC], kl[2][NC], vf[NT], vl[NT];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          const int64_t e = ((int64_t)(la * NC + c) * p.ks + c0 + 16 * h + li) * 8;
+          kf[h][c] = __builtin_bit_cast(bf16x8, ld16v(kt + e));
+          kl[h][c] = __builtin_bit_cast(bf16x8, ld16v(ktl + e));
+        }
+      }
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int64_t e = (int64_t)(16 * nt + li) * p.ks + c0 + 4 * la;  // half 0; half 1 at +16
+        const u32x2 a0 = ld8v(vt + e), a1 = ld8v(vt + e + 16);
+        const u32x2 b0 = ld8v(vtl + e), b1 = ld8v(vtl + e + 16);
+        vf[nt] = __builtin_bit_cast(bf16x8, u32x4{a0.x, a0.y, a1.x, a1.y});
+        vl[nt] = __builtin_bit_cast(bf16x8, u32x4{b0.x, b0.y, b1.x, b1.y});
+      }
+      run_unit<HD, true>(st, kf, vf, kl, vl, li, la, 32, c0, row0 + li, p.group, p.k);
     }
   }
 
-  if (t0 < t1) {
+  const int nunits = (t1 - t0 + 31) >> 5;   // 0 when the split has no cache tokens
+  if (nunits > 0) {
     const bf16* kbase = (const bf16*)p.k_base + (int64_t)g * p.k_sh;
     const bf16* vbase = (const bf16*)p.v_base + (int64_t)g * p.v_sh;
-    // A 16-token chunk starting at a multiple of 16 lies inside one block, and
-    // its first token is valid, so the block is one the sequence owns.
-    auto load_cache = [&](Frag<HD>& f, int c0) {
-      const int64_t blk = phys_block(p, b, c0);
-      load_frag<HD, true>(f, kbase + blk * p.k_sb, vbase + blk * p.v_sb, c0 & (bs - 1), bs, li, la);
+    // Unit u: halves start at t0 + 32u and t0 + 32u + 16; a half whose first
+    // token is past the end re-reads the first half (then masked), so every
+    // address lies in a block the sequence owns.
+    auto fetch = [&](Unit<HD, W>& un, int u) __attribute__((always_inline)) {
+      const int ta = t0 + 32 * u;
+      const int tb = ta + 16 < t1 ? ta + 16 : ta;
+      fetch_unit<HD, W>(un, kbase, vbase, p.k_sb, p.v_sb, phys_block(p, b, ta), phys_block(p, b, tb),
+                        ta & (bs - 1), tb & (bs - 1), bs, tid);
     };
-    // Prefetch addresses are clamped to the last full chunk, so every load
-    // stays inside the sequence.
-    const int nfull = (t1 - t0) >> 4, rem = (t1 - t0) & 15;
-    Frag<HD> buf[DEPTH];
-    if (nfull > 0) {
-#pragma unroll
-      for (int j = 0; j < DEPTH - 1; ++j) load_cache(buf[j], t0 + 16 * (j < nfull ? j : nfull - 1));
-    }
-    for (int i = 0; i < nfull; i += DEPTH) {
-#pragma unroll
-      for (int u = 0; u < DEPTH; ++u) {
-        if (i + u < nfull) {
-          const int nx = i + u + DEPTH - 1;
-          load_cache(buf[(u + DEPTH - 1) % DEPTH], t0 + 16 * (nx < nfull ? nx : nfull - 1));
-          process_chunk<HD, QT, kFull>(buf[u], qf, o, m, l, li, la, 16, 0, row0, p.group, p.k);
-        }
-      }
-    }
-    if (rem) {
-      Frag<HD> f;
-      load_cache(f, t0 + 16 * nfull);
-      process_chunk<HD, QT, kTail>(f, qf, o, m, l, li, la, rem, 0, row0, p.group, p.k);
+    auto step = [&](const Unit<HD, W>& un, int u, int buf) __attribute__((always_inline)) {
+      const int limit = t1 - (t0 + 32 * u);
+      if (limit >= 32)
+        stage_unit<HD, W, false>(un, stage[buf], limit, tid);
+      else
+        stage_unit<HD, W, true>(un, stage[buf], limit, tid);
+    };
+    // Two units in flight in registers, two LDS stages, one barrier per unit.
+    // Units go in pairs (an odd count gets one more unit, wholly past the end
+    // and therefore masked out) and every prefetch is issued, clamped to the last
+    // unit, so the loop body has no data-dependent branches around its loads.
+    const int last = nunits - 1;
+    Unit<HD, W> ua, ub;
+    fetch(ua, 0);
+    fetch(ub, min(1, last));
+    for (int u = 0; u < nunits; u += 2) {
+      step(ua, u, 0);
+      fetch(ua, min(u + 2, last));
+      __syncthreads();
+      compute_unit<HD, W>(st, stage[0], t1 - (t0 + 32 * u), li, la, row0 + li);
+      step(ub, u + 1, 1);
+      fetch(ub, min(u + 3, last));
+      __syncthreads();
+      compute_unit<HD, W>(st, stage[1], t1 - (t0 + 32 * (u + 1)), li, la, row0 + li);
     }
   }
 
   const int64_t prow = (((int64_t)b * p.n_kv + g) * p.max_splits + s) * p.r_alloc + row0;
+  float lt = st.l;
+  lt += __shfl_xor(lt, 16);
+  lt += __shfl_xor(lt, 32);
+  if (la == 0) p.ml_part[prow + li] = make_float2(st.m, lt);
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt) {
-    float lt = l[qt];
-    lt += __shfl_xor(lt, 16);
-    lt += __shfl_xor(lt, 32);
-    if (la == 0) p.ml_part[prow + 16 * qt + li] = make_float2(m[qt], lt);
+  for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        p.o_part[(prow + 16 * qt + 4 * la + r) * HD + 16 * nt + li] = o[qt][nt][r];
-  }
+    for (int r = 0; r < 4; ++r) p.o_part[(prow + 4 * la + r) * HD + 16 * nt + li] = st.o[nt][r];
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -415,19 +486,19 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
 
 }  // namespace
 
-// Prefetch depth of the production instantiation.
-constexpr int kAttnDepth = SP_ATTN_DEPTH;
-
-hipError_t launch_attention_bf16(const AttnParams& p, int hd, int qt, int batch, hipStream_t s) {
+hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
   const dim3 grid(p.max_splits, p.n_kv * p.n_qgroups, batch);
-#define SP_ATTN_CASE(HD_, QT_)                                                                  \
-  if (hd == HD_ && qt == QT_) {                                                                 \
-    hipLaunchKernelGGL((attn_split_bf16<HD_, QT_, kAttnDepth>), grid, dim3(64), 0, s, p);  \
-    return hipGetLastError();                                                                   \
+#define SP_ATTN_CASE(HD_, W_)                                                          \
+  if (hd == HD_ && waves == W_) {                                                      \
+    hipLaunchKernelGGL((attn_split_bf16<HD_, W_>), grid, dim3(64 * W_), 0, s, p);       \
+    return hipGetLastError();                                                          \
   }
   SP_ATTN_CASE(128, 1) SP_ATTN_CASE(128, 2) SP_ATTN_CASE(128, 3) SP_ATTN_CASE(128, 4)
+  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
+  SP_ATTN_CASE(128, 12) SP_ATTN_CASE(128, 16)
   SP_ATTN_CASE(64, 1) SP_ATTN_CASE(64, 2) SP_ATTN_CASE(64, 3) SP_ATTN_CASE(64, 4)
-  SP_ATTN_CASE(64, 5)
+  SP_ATTN_CASE(64, 5) SP_ATTN_CASE(64, 6) SP_ATTN_CASE(64, 8) SP_ATTN_CASE(64, 10)
+  SP_ATTN_CASE(64, 12) SP_ATTN_CASE(64, 16)
 #undef SP_ATTN_CASE
   return hipErrorInvalidValue;
 }

@@ -19,14 +19,19 @@ struct RopeParams {
   const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32
   const int* seq_lens;     // device [B]
   const int* err;          // nullable: skip everything if *err != 0
-  void* q;                 // [B][n_kv][r_alloc][hd]           (activation dtype), scaled
+  void* q;                 // [B][n_kv][r_alloc][hd], scaled by q_scale
   void* k_soft;            // [B][n_kv] tiles of ks tokens, chunked layout (x = 16 B / elem)
   void* v_soft;            // [n_kv][hd][ks] (batch-invariant)
+  // bf16 split output (dt == kBF16): q, k_soft, v_soft receive bf16(x) and these
+  // the remainders bf16(x - bf16(x)), same layouts
+  void* q_lo;
+  void* k_soft_lo;
+  void* v_soft_lo;
   int n_q, n_kv, hd, k, group, r_alloc, ks, max_seq_len;
   double rope_base;
   float q_scale;           // log2(e) / sqrt(hd)
 };
-// dt: activation dtype of the outputs (kF32 or kF16)
+// dt: output type: kF32, or kBF16 for the hi/lo bf16 split
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
@@ -34,6 +39,9 @@ struct AttnParams {
   const void* q;           // [B][n_kv][r_alloc][hd], pre-scaled by log2(e)/sqrt(hd)
   const void* k_soft;      // [B][n_kv] chunked tiles of ks tokens
   const void* v_soft;      // [n_kv][hd][ks]
+  const void* q_lo;        // bf16 path: remainders of q, k_soft, v_soft (same layouts)
+  const void* k_soft_lo;
+  const void* v_soft_lo;
   const void* k_base;
   const void* v_base;
   int64_t k_sb, k_sh, v_sb, v_sh;     // elements
@@ -45,8 +53,9 @@ struct AttnParams {
   int n_kv, group, k, rows, r_alloc, ks, n_qgroups;
   int bs_log2, mbps, max_seq_len, split_len, max_splits;
 };
-// bf16 MFMA path: head_dim 64/128, rows per wave 16*qt.
-hipError_t launch_attention_bf16(const AttnParams& p, int hd, int qt, int batch, hipStream_t s);
+// bf16-storage path (bf16 MFMA, split Q and P): head_dim 64/128, `waves` 16-row
+// query tiles per workgroup (1, 2, 3, 4, 5, 6, 8, 10, 12 or 16).
+hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s);
 // fp32 VALU path: head_dim 64/128, rows <= 64.
 hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);
 

@@ -28,7 +28,15 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, const TG* gain,
 // ---------------------------------------------------------------- RoPE + scatter
 // grid (k, n_q + 2 n_kv, B), hd/2 threads: thread i rotates the pair (i, i + hd/2)
 // of head h of soft row j by (N_b + j) * base^(-2i/hd), the angle in fp64.
-template <typename T>
+// SPLIT (T = bf16): each value x is stored as hi = bf16(x) and lo = bf16(x - hi).
+template <typename T, bool SPLIT>
+__device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
+  const T h = from_f32<T>(x);
+  ((T*)hi)[idx] = h;
+  if (SPLIT) ((T*)lo)[idx] = from_f32<T>(x - to_f32(h));
+}
+
+template <typename T, bool SPLIT>
 __global__ void rope_scatter(const RopeParams p) {
   const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
   if (p.err && *p.err) return;
@@ -37,9 +45,9 @@ __global__ void rope_scatter(const RopeParams p) {
   if (h >= p.n_q + p.n_kv) {  // value head: no rotation, the same for every sequence
     if (b != 0) return;
     const int g = h - p.n_q - p.n_kv;
-    T* vt = (T*)p.v_soft + (int64_t)g * hd * p.ks;
-    vt[(int64_t)i * p.ks + j] = from_f32<T>(row[h * hd + i]);
-    vt[(int64_t)(i + half) * p.ks + j] = from_f32<T>(row[h * hd + i + half]);
+    const int64_t base = (int64_t)g * hd * p.ks;
+    put<T, SPLIT>(p.v_soft, p.v_soft_lo, base + (int64_t)i * p.ks + j, row[h * hd + i]);
+    put<T, SPLIT>(p.v_soft, p.v_soft_lo, base + (int64_t)(i + half) * p.ks + j, row[h * hd + i + half]);
     return;
   }
   int n = p.seq_lens[b];
@@ -51,16 +59,16 @@ __global__ void rope_scatter(const RopeParams p) {
   const float r0 = x0 * c - x1 * s, r1 = x1 * c + x0 * s;
   if (h < p.n_q) {
     const int g = h / p.group, rr = j * p.group + h % p.group;
-    T* q = (T*)p.q + (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
-    q[i] = from_f32<T>(r0 * p.q_scale);
-    q[i + half] = from_f32<T>(r1 * p.q_scale);
+    const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
+    put<T, SPLIT>(p.q, p.q_lo, base + i, r0 * p.q_scale);
+    put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
   } else {
     constexpr int X = 16 / sizeof(T);
     const int g = h - p.n_q;
-    T* kt = (T*)p.k_soft + ((int64_t)b * p.n_kv + g) * p.ks * hd;
+    const int64_t base = ((int64_t)b * p.n_kv + g) * p.ks * hd;
     const int i1 = i + half;
-    kt[((int64_t)(i / X) * p.ks + j) * X + i % X] = from_f32<T>(r0);
-    kt[((int64_t)(i1 / X) * p.ks + j) * X + i1 % X] = from_f32<T>(r1);
+    put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + ((int64_t)(i / X) * p.ks + j) * X + i % X, r0);
+    put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + ((int64_t)(i1 / X) * p.ks + j) * X + i1 % X, r1);
   }
 }
 
@@ -135,10 +143,10 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
 
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s) {
   const dim3 grid(p.k, p.n_q + 2 * p.n_kv, batch), block(p.hd / 2);
-  if (dt == kF16)
-    hipLaunchKernelGGL(rope_scatter<f16>, grid, block, 0, s, p);
+  if (dt == kBF16)
+    hipLaunchKernelGGL((rope_scatter<bf16, true>), grid, block, 0, s, p);
   else if (dt == kF32)
-    hipLaunchKernelGGL(rope_scatter<float>, grid, block, 0, s, p);
+    hipLaunchKernelGGL((rope_scatter<float, false>), grid, block, 0, s, p);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

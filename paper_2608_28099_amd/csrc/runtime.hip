@@ -25,10 +25,10 @@ int ilog2(int64_t x) { int r = 0; while ((int64_t(1) << r) < x) ++r; return r; }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 struct Plan {
-  int group, rows, qt, n_qgroups, r_alloc, ks, nqkv, split_len, max_splits, esz;
+  int group, rows, waves, n_qgroups, r_alloc, ks, nqkv, split_len, max_splits, esz;
   // workspace offsets (bytes)
-  size_t off_u, off_qkv, off_q, off_ksoft, off_vsoft, off_opart, off_ml, off_attn, off_a, off_w,
-      off_s, off_y, off_err, total;
+  size_t off_u, off_qkv, off_q, off_ksoft, off_vsoft, off_q_lo, off_ksoft_lo, off_vsoft_lo,
+      off_opart, off_ml, off_attn, off_a, off_w, off_s, off_y, off_err, total;
 };
 
 int check_config(const sp_probe_config* c) {
@@ -58,17 +58,23 @@ Plan make_plan(const sp_probe_config& c) {
   p.rows = c.k * p.group;
   const int tiles = (p.rows + 15) / 16;
   if (c.dtype == SP_F32) {
-    p.qt = 0;
+    p.waves = 0;
     p.n_qgroups = 1;
     p.r_alloc = p.rows;
   } else {
-    // rows per wave: at most 64 at head_dim 128 (register budget), 80 at 64;
-    // the groups are as even as possible
-    const int max_qt = c.head_dim == 128 ? 4 : 5;
-    const int groups = (tiles + max_qt - 1) / max_qt;
-    p.qt = (tiles + groups - 1) / groups;
-    p.n_qgroups = (tiles + p.qt - 1) / p.qt;
-    p.r_alloc = p.n_qgroups * p.qt * 16;
+    // one wave per 16-row query tile, at most 8 (head_dim 128) or 16 (64) waves
+    // per workgroup, whose register budget then still fits without spills; the
+    // sizes below are the instantiated ones (extra tiles are padding)
+    static const int kWaves[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
+    const int max_w = c.head_dim == 128 ? 8 : 16;
+    const int groups = (tiles + max_w - 1) / max_w;
+    const int per_group = (tiles + groups - 1) / groups;
+    int w = max_w;
+    for (int cand : kWaves)
+      if (cand >= per_group) { w = cand; break; }
+    p.waves = w;
+    p.n_qgroups = (tiles + w - 1) / w;
+    p.r_alloc = p.n_qgroups * w * 16;
   }
   p.ks = ((c.k + 31) / 32) * 32;
   p.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
@@ -91,6 +97,11 @@ Plan make_plan(const sp_probe_config& c) {
   p.off_q = take(B * c.n_kv_heads * p.r_alloc * hd * e);
   p.off_ksoft = take(B * c.n_kv_heads * p.ks * hd * e);
   p.off_vsoft = take((size_t)c.n_kv_heads * hd * p.ks * e);
+  // remainders of the split bf16 queries and soft keys/values (bf16 storage only)
+  const size_t lo = c.dtype == SP_BF16 ? 1 : 0;
+  p.off_q_lo = take(lo * B * c.n_kv_heads * p.r_alloc * hd * e);
+  p.off_ksoft_lo = take(lo * B * c.n_kv_heads * p.ks * hd * e);
+  p.off_vsoft_lo = take(lo * (size_t)c.n_kv_heads * hd * p.ks * e);
   p.off_opart = take(B * c.n_kv_heads * p.max_splits * p.r_alloc * hd * 4);
   p.off_ml = take(B * c.n_kv_heads * p.max_splits * p.r_alloc * 8);
   p.off_attn = take(M * c.n_q_heads * hd * e);
@@ -282,11 +293,14 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     r.q = at<void>(h, pl.off_q);
     r.k_soft = at<void>(h, pl.off_ksoft);
     r.v_soft = at<void>(h, pl.off_vsoft);
+    r.q_lo = at<void>(h, pl.off_q_lo);
+    r.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
+    r.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
     r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = c.k; r.group = pl.group;
     r.r_alloc = pl.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
     r.rope_base = c.rope_base;
     r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
-    SP_TRY(launch_rope_scatter(at_dt, r, B, s));
+    SP_TRY(launch_rope_scatter(dt, r, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
@@ -295,6 +309,9 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   ap.q = at<void>(h, pl.off_q);
   ap.k_soft = at<void>(h, pl.off_ksoft);
   ap.v_soft = at<void>(h, pl.off_vsoft);
+  ap.q_lo = at<void>(h, pl.off_q_lo);
+  ap.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
+  ap.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
   ap.k_base = kv->k_base; ap.v_base = kv->v_base;
   ap.k_sb = kv->k_stride_block; ap.k_sh = kv->k_stride_head;
   ap.v_sb = kv->v_stride_block; ap.v_sh = kv->v_stride_head;
@@ -308,7 +325,7 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   ap.bs_log2 = ilog2(kv->block_size); ap.mbps = kv->max_blocks_per_seq;
   ap.max_seq_len = c.max_seq_len; ap.split_len = pl.split_len; ap.max_splits = pl.max_splits;
   if (dt == kBF16)
-    SP_TRY(launch_attention_bf16(ap, hd, pl.qt, B, s));
+    SP_TRY(launch_attention_bf16(ap, hd, pl.waves, B, s));
   else
     SP_TRY(launch_attention_f32(ap, hd, B, s));
   if (!mark()) return SP_ERR_HIP;
