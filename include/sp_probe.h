@@ -86,7 +86,7 @@ typedef struct sp_probe_config {
   int32_t max_batch;     /* largest batch a forward may pass */
   int32_t max_seq_len;   /* largest context length N_b a forward may pass (debug mode checks it;
                             otherwise larger values are clamped to it) */
-  int32_t split_len;     /* tokens per attention split, a power of two >= 256; 0 = automatic */
+  int32_t split_len;     /* tokens per attention split, a power of two in [256, 16384]; 0 = automatic */
   int32_t flags;         /* SP_FLAG_* */
 } sp_probe_config;
 

@@ -15,6 +15,9 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden",
     # packed fp32 instructions are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # matrix-core accumulators in ordinary VGPRs: the attention state is rescaled
+    # and masked by VALU code, and AGPR accumulators cost a copy each way
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

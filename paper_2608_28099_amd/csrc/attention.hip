@@ -59,18 +59,18 @@ struct RowState {
   float m, l;             // reference max of row li (log2 units); this lane's part of its sum
 };
 
-// One 32-token unit for one wave.  kf[h][c]: K[token li of half h][8 (la*NC + c) ..];
-// vf[nt]: V[tokens 4la..4la+3 of half 0, then of half 1][16nt + li].  SOFT: the soft keys,
-// whose K and V are themselves hi + lo pairs (kl, vl) and whose visibility is
-// causal; cache units mask keys at or past `limit`.
+// One 32-token unit for one wave, in two phases.  qk_unit: kf[h][c] =
+// K[token pi_h(li)][8 (la*NC + c) ..] (the unit layout below); score i of the
+// lane (i = 4h + r) is token 8la + i for query li.  softmax_pv_unit: vf[nt] =
+// V[tokens 8la..8la+7][16nt + li].  SOFT: the soft keys, whose K and V are
+// themselves hi + lo pairs (kl, vl) and whose visibility is causal; cache units
+// mask keys at or past `limit`.
 template <int HD, bool SOFT>
-__device__ __forceinline__ void run_unit(RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
-                                         const bf16x8 (&vf)[HD / 16],
-                                         const bf16x8 (&kl)[2][HD / 32],
-                                         const bf16x8 (&vl)[HD / 16], int li, int la,
-                                         int limit, int key0, int row, int group, int k) {
-  constexpr int NC = HD / 32, NT = HD / 16;
-  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+__device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
+                                        const bf16x8 (&kl)[2][HD / 32], f32x4& s0, f32x4& s1) {
+  constexpr int NC = HD / 32;
+  s0 = f32x4{0.f, 0.f, 0.f, 0.f};
+  s1 = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     s0 = mfma16x16x32_bf16(kf[0][c], st.qh[c], s0);
@@ -82,6 +82,14 @@ __device__ __forceinline__ void run_unit(RowState<HD>& st, const bf16x8 (&kf)[2]
       s1 = mfma16x16x32_bf16(kl[1][c], st.qh[c], s1);
     }
   }
+}
+
+template <int HD, bool SOFT>
+__device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x4 s1,
+                                                const bf16x8 (&vf)[HD / 16],
+                                                const bf16x8 (&vl)[HD / 16], int li, int la,
+                                                int limit, int key0, int row, int group, int k) {
+  constexpr int NT = HD / 16;
   float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
   if (SOFT) {
     // soft key j' is visible to query row r iff j' <= r / G (causal, own row included)
@@ -89,11 +97,11 @@ __device__ __forceinline__ void run_unit(RowState<HD>& st, const bf16x8 (&kf)[2]
     jmax = jmax < k - 1 ? jmax : k - 1;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      if (key0 + 16 * (i >> 2) + 4 * la + (i & 3) > jmax) sc[i] = -INFINITY;
+      if (key0 + 8 * la + i > jmax) sc[i] = -INFINITY;
   } else if (limit < 32) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      if (16 * (i >> 2) + 4 * la + (i & 3) >= limit) sc[i] = -INFINITY;
+      if (8 * la + i >= limit) sc[i] = -INFINITY;
   }
   float lmax = sc[0];
 #pragma unroll
@@ -135,106 +143,134 @@ __device__ __forceinline__ void run_unit(RowState<HD>& st, const bf16x8 (&kf)[2]
   }
 }
 
-// Pieces of a 32-token unit, as fetched: 16 bytes each; for half h (16 tokens),
-// KP pieces of the K tile (piece c8*16 + t: head dims 8 c8 .. 8 c8 + 7 of
-// token t) followed by KP pieces of the V tile (piece 2 i + e: tokens
-// 8e .. 8e + 7 of head dim i).
-// LDS stage layout: K as fetched, [h][c8][t] in 16-byte pieces (index
-// h*KP + c8*16 + t); then V in 8-byte quads of 4 tokens, ordered
-// [nt][la][li][h] with head dim i = 16 nt + li and tokens 4 la .. 4 la + 3 of
-// half h, so the PV operand of lane (li, la) -- tokens 4la..4la+3 of both
-// halves -- is 16 contiguous bytes and a wave's read is 1 KB contiguous.
-template <int HD, int W>
-struct Unit {
-  static constexpr int KP = 2 * HD;                       // pieces per half per tensor
-  static constexpr int NP = 4 * KP;                       // pieces per unit
-  static constexpr int PPL = (NP + 64 * W - 1) / (64 * W);  // pieces per lane
-  static constexpr bool EXACT = NP % (64 * W) == 0;       // every lane has PPL pieces
-  u32x4 r[PPL];
+// LDS image of a 32-token unit, in 16-byte pieces.  Token T of the unit lies
+// in half T >> 4 (16 tokens inside one block, slots t = T & 15).  The QK
+// product of half-MFMA h (h = 0, 1) takes, as its row m, token
+//   pi_h(m) = 8 (m >> 2) + 4 h + (m & 3),
+// so that lane (li, la) receives scores of tokens 8 la + 4 h + r, i.e. tokens
+// 8 la .. 8 la + 7 over both half-MFMAs: exactly its A operand of the PV MFMA.
+// Pieces are grouped by half, so that each 64-piece wave-instruction of the
+// direct loads reads from one block:
+//   K half hh: piece hh * KHP + c8 * 16 + t = K[16 hh + t][8 c8 .. 8 c8 + 7]
+//   V half hh: piece VB + hh * 2 HD + (2 nt + e) * 16 + li
+//                    = V[16 hh + 8 e .. 16 hh + 8 e + 7][16 nt + li]
+// A K fragment read (16 lanes: tokens pi_h(0..15), 8 from each half) then
+// covers 16 distinct 16-byte bank groups thanks to the 4-piece pad of the
+// second K half; a V fragment read is 256 contiguous bytes per 16 lanes.
+template <int HD>
+struct UnitLayout {
+  static constexpr int NI = HD / 8;           // wave-instructions (64 pieces each) per unit
+  static constexpr int IPG = HD / 32;         // wave-instructions per (tensor, half) group
+  static constexpr int KHP = 2 * HD + 4;      // K half pitch (pieces), padded
+  static constexpr int VB = KHP + 2 * HD;     // first V piece
+  static constexpr int PIECES = VB + 4 * HD;  // pieces per stage
+  // first piece of group gi (0: K half 0, 1: K half 1, 2: V half 0, 3: V half 1)
+  static constexpr __device__ int group_base(int gi) {
+    return gi == 0 ? 0 : gi == 1 ? KHP : gi == 2 ? VB : VB + 2 * HD;
+  }
+  static __device__ __forceinline__ int k_piece(int h, int c8, int li) {
+    const int tk = 8 * (li >> 2) + 4 * h + (li & 3);
+    return (tk >> 4) * KHP + c8 * 16 + (tk & 15);
+  }
+  static __device__ __forceinline__ int v_piece(int nt, int li, int la) {
+    return VB + (la >> 1) * 2 * HD + (2 * nt + (la & 1)) * 16 + li;
+  }
 };
 
-// Issue the unit's loads.  blk0/blk1, slot0/slot1: block and first slot of each half.
-template <int HD, int W>
-__device__ __forceinline__ void fetch_unit(Unit<HD, W>& un, const bf16* kbase, const bf16* vbase,
-                                           int64_t k_sb, int64_t v_sb, int64_t blk0, int64_t blk1,
-                                           int slot0, int slot1, int bs, int tid) {
-  using U = Unit<HD, W>;
-#pragma unroll
-  for (int j = 0; j < U::PPL; ++j) {
-    const int pc = tid + j * 64 * W;
-    if (U::EXACT || pc < U::NP) {
-      const int h = pc >= 2 * U::KP;
-      const int q = pc - h * 2 * U::KP;
-      const int64_t blk = h ? blk1 : blk0;
-      const int slot = h ? slot1 : slot0;
-      const bf16* a = q < U::KP
-          ? kbase + blk * k_sb + ((int64_t)(q >> 4) * bs + slot + (q & 15)) * 8
-          : vbase + blk * v_sb + (int64_t)((q - U::KP) >> 1) * bs + slot + 8 * ((q - U::KP) & 1);
-      un.r[j] = ld16v_stream(a);
-    }
-  }
+// Direct global -> LDS load of 16 bytes per lane from base + lane_off (base
+// uniform across the wave, in SGPRs): lane l's bytes land at wave_dst + 16 l
+// (wave_dst uniform, in M0).  Streaming (nt).  Written as inline asm so that
+// the compiler does not order later LDS reads after it with a full vmcnt(0):
+// the kernel waits for these loads itself (wait_vmcnt, then lds_barrier).  The
+// vector-memory counter retires in order, so loads the compiler does not count
+// only make its own waits for other loads stricter.
+__device__ __forceinline__ void ld16_to_lds(const void* base, uint32_t lane_off, u32x4* wave_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u32x4*)wave_dst;
+  asm volatile("global_load_lds_dwordx4 %0, %1 nt" : : "v"(lane_off), "s"(base), "{m0}"(lds) : "memory");
 }
 
-// Write the fetched unit into an LDS stage (layout above).  TAIL: slots at or
-// past `limit` are zeroed (their bytes may be anything, NaN included).
-template <int HD, int W, bool TAIL>
-__device__ __forceinline__ void stage_unit(const Unit<HD, W>& un, u32x4* dst, int limit, int tid) {
-  using U = Unit<HD, W>;
-  u32x2* vdst = reinterpret_cast<u32x2*>(dst + 2 * U::KP);
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Workgroup barrier for LDS traffic: waits for this wave's LDS operations
+// (lgkmcnt) but not for its outstanding global loads, so direct-to-LDS loads of
+// later units stay in flight; the caller first waits (vmcnt) for those that must
+// have landed.  The empty asm statements keep the compiler from moving memory
+// accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Longest split of the bf16 path: its physical block ids are staged in LDS.
+constexpr int kMaxSplitBf16 = 16384;
+constexpr int kMaxSplitBlocks = kMaxSplitBf16 / 16 + 1;  // block size >= 16, t0 maybe mid-block
+
+// Zero the V values of tokens at or past `limit` in a staged tail unit (the
+// bytes there may be anything, NaN included, and P V would carry 0 * NaN).
+template <int HD, int W>
+__device__ __forceinline__ void zero_tail(u32x4* sb, int limit, int tid) {
+  u32x4* v = sb + UnitLayout<HD>::VB;
+  for (int q = tid; q < 4 * HD; q += 64 * W) {
+    const int tk0 = 16 * (q / (2 * HD)) + 8 * ((q >> 4) & 1);  // first of the piece's 8 tokens
+    if (tk0 + 8 > limit) {
+      u32x4 x = v[q];
 #pragma unroll
-  for (int j = 0; j < U::PPL; ++j) {
-    const int pc = tid + j * 64 * W;
-    if (U::EXACT || pc < U::NP) {
-      u32x4 v = un.r[j];
-      const int h = pc >= 2 * U::KP;
-      const int q = pc - h * 2 * U::KP;
-      if (q < U::KP) {
-        if (TAIL && 16 * h + (q & 15) >= limit) v = u32x4{0u, 0u, 0u, 0u};
-        dst[h * U::KP + q] = v;
-      } else {
-        const int i = (q - U::KP) >> 1, e = (q - U::KP) & 1;
-        if (TAIL) {
-          const int tk0 = 16 * h + 8 * e;  // first of the piece's 8 tokens
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int keep = limit - (tk0 + 2 * w);
-            v[w] &= keep >= 2 ? 0xffffffffu : (keep == 1 ? 0x0000ffffu : 0u);
-          }
-        }
-        const int nt = i >> 4, li = i & 15;
-        vdst[((nt * 4 + 2 * e) * 16 + li) * 2 + h] = u32x2{v.x, v.y};      // tokens 8e .. 8e + 3
-        vdst[((nt * 4 + 2 * e + 1) * 16 + li) * 2 + h] = u32x2{v.z, v.w};  // tokens 8e + 4 .. 8e + 7
+      for (int w = 0; w < 4; ++w) {
+        const int keep = limit - (tk0 + 2 * w);
+        x[w] &= keep >= 2 ? 0xffffffffu : (keep == 1 ? 0x0000ffffu : 0u);
       }
+      v[q] = x;
     }
   }
 }
 
 // A wave's fragments of a staged unit, then the unit's softmax and products.
-template <int HD, int W>
+template <int HD>
 __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, int limit, int li,
                                              int la, int row) {
-  constexpr int NC = HD / 32, NT = HD / 16, KP = Unit<HD, W>::KP;
-  bf16x8 kf[2][NC], vf[NT];
+  constexpr int NC = HD / 32, NT = HD / 16;
+  f32x4 s0, s1;
+  {
+    bf16x8 kf[2][NC];
 #pragma unroll
-  for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
-      kf[h][c] = __builtin_bit_cast(bf16x8, sb[h * KP + (la * NC + c) * 16 + li]);
+      for (int c = 0; c < NC; ++c)
+        kf[h][c] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::k_piece(h, la * NC + c, li)]);
+    qk_unit<HD, false>(st, kf, kf, s0, s1);
+  }
+  // V fragments are read only once the QK products are issued, into the
+  // registers the K fragments held.
+  __builtin_amdgcn_sched_barrier(0);
+  bf16x8 vf[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
-    vf[nt] = __builtin_bit_cast(bf16x8, sb[2 * KP + (nt * 4 + la) * 16 + li]);
-  run_unit<HD, false>(st, kf, vf, kf, vf, li, la, limit, 0, row, 1, 1);
+    vf[nt] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::v_piece(nt, li, la)]);
+  softmax_pv_unit<HD, false>(st, s0, s1, vf, vf, li, la, limit, 0, row, 1, 1);
 }
 
-// W waves per workgroup, one per 16-row query tile.
+// W waves per workgroup, one per 16-row query tile.  Three LDS stages: unit u
+// is computed from stage u % 3 while units u + 1 and u + 2 are in flight.
 template <int HD, int W>
 __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   constexpr int NC = HD / 32, NT = HD / 16;
-  using U = Unit<HD, W>;
-  __shared__ u32x4 stage[2][U::NP];
+  constexpr int NI = UnitLayout<HD>::NI;
+  constexpr int PPL = (NI + W - 1) / W;  // wave-instructions per wave per unit
+  static_assert(W <= 2 * NI, "a wave must have at least one distinct instruction slot");
+  __shared__ u32x4 stage[3][UnitLayout<HD>::PIECES];
+  __shared__ int blk_ids[kMaxSplitBlocks];   // physical block of each logical block of the split
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, la = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, la = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   __builtin_assume(tid < 64 * W);
+  __builtin_assume(wave >= 0 && wave < W);
   const int s = blockIdx.x;
   const int g = blockIdx.y / p.n_qgroups, qg = blockIdx.y % p.n_qgroups;
   const int b = blockIdx.z;
@@ -261,30 +297,36 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   }
 
   if (s == 0) {
-    // the soft keys: hi/lo bf16 tiles of ks tokens (a multiple of 32), read in place
+    // the soft keys: hi/lo bf16 tiles of ks tokens (a multiple of 32), read in
+    // place with the unit's token order
     const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * HD, vo = (int64_t)g * HD * p.ks;
     const bf16 *kt = (const bf16*)p.k_soft + ko, *ktl = (const bf16*)p.k_soft_lo + ko;
     const bf16 *vt = (const bf16*)p.v_soft + vo, *vtl = (const bf16*)p.v_soft_lo + vo;
     for (int c0 = 0; c0 < p.k; c0 += 32) {
-      bf16x8 kf[2][NC], kl[2][NC], vf[NT], vl[NT];
+      f32x4 s0, s1;
+      {
+        bf16x8 kf[2][NC], kl[2][NC];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 2; ++h) {
+          const int tk = c0 + 8 * (li >> 2) + 4 * h + (li & 3);
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-          const int64_t e = ((int64_t)(la * NC + c) * p.ks + c0 + 16 * h + li) * 8;
-          kf[h][c] = __builtin_bit_cast(bf16x8, ld16v(kt + e));
-          kl[h][c] = __builtin_bit_cast(bf16x8, ld16v(ktl + e));
+          for (int c = 0; c < NC; ++c) {
+            const int64_t e = ((int64_t)(la * NC + c) * p.ks + tk) * 8;
+            kf[h][c] = __builtin_bit_cast(bf16x8, ld16v(kt + e));
+            kl[h][c] = __builtin_bit_cast(bf16x8, ld16v(ktl + e));
+          }
         }
+        qk_unit<HD, true>(st, kf, kl, s0, s1);
       }
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8 vf[NT], vl[NT];
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
-        const int64_t e = (int64_t)(16 * nt + li) * p.ks + c0 + 4 * la;  // half 0; half 1 at +16
-        const u32x2 a0 = ld8v(vt + e), a1 = ld8v(vt + e + 16);
-        const u32x2 b0 = ld8v(vtl + e), b1 = ld8v(vtl + e + 16);
-        vf[nt] = __builtin_bit_cast(bf16x8, u32x4{a0.x, a0.y, a1.x, a1.y});
-        vl[nt] = __builtin_bit_cast(bf16x8, u32x4{b0.x, b0.y, b1.x, b1.y});
+        const int64_t e = (int64_t)(16 * nt + li) * p.ks + c0 + 8 * la;
+        vf[nt] = __builtin_bit_cast(bf16x8, ld16v(vt + e));
+        vl[nt] = __builtin_bit_cast(bf16x8, ld16v(vtl + e));
       }
-      run_unit<HD, true>(st, kf, vf, kl, vl, li, la, 32, c0, row0 + li, p.group, p.k);
+      softmax_pv_unit<HD, true>(st, s0, s1, vf, vl, li, la, 32, c0, row0 + li, p.group, p.k);
     }
   }
 
@@ -292,39 +334,76 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   if (nunits > 0) {
     const bf16* kbase = (const bf16*)p.k_base + (int64_t)g * p.k_sh;
     const bf16* vbase = (const bf16*)p.v_base + (int64_t)g * p.v_sh;
+    const int lb0 = t0 >> p.bs_log2;
+    const int nlb = ((t1 - 1) >> p.bs_log2) - lb0 + 1;
+    for (int i = tid; i < min(nlb, kMaxSplitBlocks); i += 64 * W)
+      blk_ids[i] = p.block_table ? p.block_table[(int64_t)b * p.mbps + lb0 + i] : b * p.mbps + lb0 + i;
+    // Nothing the compiler tracks stays in flight past this point (the Q loads
+    // included), so it never waits on the vector-memory counter inside the loop,
+    // where the counter also holds the direct-to-LDS loads.
+    wait_vmcnt<0>();
+    lds_barrier();
+    // This wave's wave-instructions: slots j*W + wave (mod NI, so a wave count
+    // that does not divide NI re-issues a few slots; the copies carry the same
+    // bytes).  Slot sl reads group gi = sl / IPG (K or V of one half); the lane's
+    // byte offset inside that half's tile and the slot's place in the stage do
+    // not change from unit to unit, only the four group bases do.  When W
+    // divides IPG, the group of each j is a compile-time constant.
+    using L = UnitLayout<HD>;
+    constexpr bool kStaticGroups = L::IPG % W == 0;
+    uint32_t lane_off[PPL];
+    int gsel[PPL], lds_piece[PPL];
+#pragma unroll
+    for (int j = 0; j < PPL; ++j) {
+      const int slot = (j * W + wave) % NI;
+      gsel[j] = kStaticGroups ? j * W / L::IPG : slot / L::IPG;
+      lds_piece[j] = L::group_base(gsel[j]) + (slot % L::IPG) * 64;
+      const int q = (slot % L::IPG) * 64 + lane;  // piece inside its group
+      if (gsel[j] < 2)
+        lane_off[j] = (uint32_t)(((q >> 4) * bs + (q & 15)) * 16);                       // K: c8, t
+      else
+        lane_off[j] = (uint32_t)((16 * (q >> 5) + (q & 15)) * bs * 2 + ((q >> 4) & 1) * 16);  // V: i, e
+    }
     // Unit u: halves start at t0 + 32u and t0 + 32u + 16; a half whose first
     // token is past the end re-reads the first half (then masked), so every
     // address lies in a block the sequence owns.
-    auto fetch = [&](Unit<HD, W>& un, int u) __attribute__((always_inline)) {
+    auto issue = [&](int u, int buf) __attribute__((always_inline)) {
       const int ta = t0 + 32 * u;
       const int tb = ta + 16 < t1 ? ta + 16 : ta;
-      fetch_unit<HD, W>(un, kbase, vbase, p.k_sb, p.v_sb, phys_block(p, b, ta), phys_block(p, b, tb),
-                        ta & (bs - 1), tb & (bs - 1), bs, tid);
+      const int64_t ba = __builtin_amdgcn_readfirstlane(blk_ids[(ta >> p.bs_log2) - lb0]);
+      const int64_t bb = __builtin_amdgcn_readfirstlane(blk_ids[(tb >> p.bs_log2) - lb0]);
+      const int sa = ta & (bs - 1), sbb = tb & (bs - 1);
+      const bf16* g0 = kbase + ba * p.k_sb + sa * 8;
+      const bf16* g1 = kbase + bb * p.k_sb + sbb * 8;
+      const bf16* g2 = vbase + ba * p.v_sb + sa;
+      const bf16* g3 = vbase + bb * p.v_sb + sbb;
+#pragma unroll
+      for (int j = 0; j < PPL; ++j) {
+        const int gi = gsel[j];
+        const bf16* gb = gi == 0 ? g0 : gi == 1 ? g1 : gi == 2 ? g2 : g3;
+        ld16_to_lds(gb, lane_off[j], &stage[buf][lds_piece[j]]);
+      }
     };
-    auto step = [&](const Unit<HD, W>& un, int u, int buf) __attribute__((always_inline)) {
-      const int limit = t1 - (t0 + 32 * u);
-      if (limit >= 32)
-        stage_unit<HD, W, false>(un, stage[buf], limit, tid);
-      else
-        stage_unit<HD, W, true>(un, stage[buf], limit, tid);
-    };
-    // Two units in flight in registers, two LDS stages, one barrier per unit.
-    // Units go in pairs (an odd count gets one more unit, wholly past the end
-    // and therefore masked out) and every prefetch is issued, clamped to the last
-    // unit, so the loop body has no data-dependent branches around its loads.
     const int last = nunits - 1;
-    Unit<HD, W> ua, ub;
-    fetch(ua, 0);
-    fetch(ub, min(1, last));
-    for (int u = 0; u < nunits; u += 2) {
-      step(ua, u, 0);
-      fetch(ua, min(u + 2, last));
-      __syncthreads();
-      compute_unit<HD, W>(st, stage[0], t1 - (t0 + 32 * u), li, la, row0 + li);
-      step(ub, u + 1, 1);
-      fetch(ub, min(u + 3, last));
-      __syncthreads();
-      compute_unit<HD, W>(st, stage[1], t1 - (t0 + 32 * (u + 1)), li, la, row0 + li);
+    issue(0, 0);
+    if (last >= 1) issue(1, 1);
+    int buf = 0;
+    for (int u = 0; u < nunits; ++u) {
+      // this wave's loads of unit u are done once at most those of unit u + 1 remain
+      if (u < last)
+        wait_vmcnt<PPL>();
+      else
+        wait_vmcnt<0>();
+      // every wave's loads of unit u have landed and every wave is done with unit u - 1
+      lds_barrier();
+      const int limit = t1 - (t0 + 32 * u);
+      if (limit < 32) {
+        zero_tail<HD, W>(stage[buf], limit, tid);
+        lds_barrier();
+      }
+      if (u + 2 <= last) issue(u + 2, buf == 0 ? 2 : buf - 1);
+      compute_unit<HD>(st, stage[buf], limit, li, la, row0 + li);
+      buf = buf == 2 ? 0 : buf + 1;
     }
   }
 
@@ -487,6 +566,7 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
 }  // namespace
 
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
+  if (p.split_len > kMaxSplitBf16 || p.bs_log2 < 4) return hipErrorInvalidValue;
   const dim3 grid(p.max_splits, p.n_kv * p.n_qgroups, batch);
 #define SP_ATTN_CASE(HD_, W_)                                                          \
   if (hd == HD_ && waves == W_) {                                                      \
@@ -494,8 +574,7 @@ hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int bat
     return hipGetLastError();                                                          \
   }
   SP_ATTN_CASE(128, 1) SP_ATTN_CASE(128, 2) SP_ATTN_CASE(128, 3) SP_ATTN_CASE(128, 4)
-  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
-  SP_ATTN_CASE(128, 12) SP_ATTN_CASE(128, 16)
+  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8)
   SP_ATTN_CASE(64, 1) SP_ATTN_CASE(64, 2) SP_ATTN_CASE(64, 3) SP_ATTN_CASE(64, 4)
   SP_ATTN_CASE(64, 5) SP_ATTN_CASE(64, 6) SP_ATTN_CASE(64, 8) SP_ATTN_CASE(64, 10)
   SP_ATTN_CASE(64, 12) SP_ATTN_CASE(64, 16)

@@ -40,7 +40,8 @@ int check_config(const sp_probe_config* c) {
     return SP_ERR_INVALID_ARG;
   if (c->n_q_heads % c->n_kv_heads) return SP_ERR_INVALID_ARG;
   if (!(c->rms_eps >= 0.0f) || !(c->rope_base > 0.0)) return SP_ERR_INVALID_ARG;
-  if (c->split_len != 0 && (c->split_len < 256 || !is_pow2(c->split_len))) return SP_ERR_INVALID_ARG;
+  if (c->split_len != 0 && (c->split_len < 256 || c->split_len > 16384 || !is_pow2(c->split_len)))
+    return SP_ERR_INVALID_ARG;
   if (c->flags & ~(SP_FLAG_DEBUG | SP_FLAG_PROFILE)) return SP_ERR_INVALID_ARG;
   if (c->head_dim != 64 && c->head_dim != 128) return SP_ERR_UNSUPPORTED;
   if (c->k > 64 || c->n_classes > 64) return SP_ERR_UNSUPPORTED;
