@@ -101,4 +101,42 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
+// ---------------------------------------------------------------- direct loads into LDS
+// Direct global -> LDS load of 16 bytes per lane from base + lane_off (base
+// uniform across the wave, in SGPRs): lane l's bytes land at wave_dst + 16 l
+// (wave_dst uniform, in M0).  STREAM: non-temporal, for data read once (the KV
+// cache); otherwise the lines stay cached for other workgroups (weights and
+// activations of the projections).  Written as inline asm so that the compiler
+// does not order later LDS reads after it with a full vmcnt(0): the kernel
+// waits for these loads itself (wait_vmcnt, then lds_barrier).  The
+// vector-memory counter retires in order, so loads the compiler does not count
+// only make its own waits for other loads stricter.
+template <bool STREAM = true>
+__device__ __forceinline__ void ld16_to_lds(const void* base, uint32_t lane_off, u32x4* wave_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) u32x4*)wave_dst;
+  if (STREAM)
+    asm volatile("global_load_lds_dwordx4 %0, %1 nt" : : "v"(lane_off), "s"(base), "{m0}"(lds) : "memory");
+  else
+    asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(lane_off), "s"(base), "{m0}"(lds) : "memory");
+}
+
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// Workgroup barrier for LDS traffic: waits for this wave's LDS operations
+// (lgkmcnt) but not for its outstanding global loads, so direct-to-LDS loads of
+// later units stay in flight; the caller first waits (vmcnt) for those that must
+// have landed.  The empty asm statements keep the compiler from moving memory
+// accesses across the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 }  // namespace sp

@@ -1,12 +1,15 @@
 // Projections of the probe's decoder layer: C = A W^T with A [M][K] and the
 // weight W [N][K] both K-contiguous, fused epilogues (residual adds, SwiGLU).
 //
-// bf16 path: fp16 activations A, bf16 weights converted exactly to fp16 while
-// they are staged into LDS (|w| in [2^-14, 65504]), v_mfma_f32_16x16x32_f16 with
-// fp32 accumulation.  256 threads as 2 x 2 waves, a BM x BN x 64 tile staged in
-// LDS (rows padded by 16 bytes so the 16 lanes of an MFMA fragment read hit
-// distinct banks), two LDS buffers: the next K-step is fetched into registers
-// while the current one runs on the matrix cores.
+// bf16 path: fp16 activations A, bf16 weights, v_mfma_f32_16x16x32_f16 with
+// fp32 accumulation.  A workgroup computes a BM x BN tile with WGM x WGN waves
+// (each a (BM/WGM) x (BN/WGN) sub-tile) and consumes K in steps of 32 (one MFMA
+// deep).  Each step's A and W tiles are loaded straight into LDS, S - 1 steps
+// ahead of use, through an S-stage ring (one barrier per step); weights stay
+// bf16 in LDS and are converted exactly to fp16 (|w| in [2^-14, 65504]) as a
+// wave reads its fragments.  A row of a stage tile is 32 values = four 16-byte
+// pieces; piece kp of row r sits at r * 4 + (kp ^ ((r >> 2) & 3)), so the 16
+// lanes that read piece kp of 16 consecutive rows hit 16 distinct bank groups.
 // SwiGLU: the BN weight rows of a tile alternate 16 gate rows and the 16
 // matching up rows, so every lane holds gate and up of the same outputs.
 #include "common.h"
@@ -15,66 +18,76 @@
 namespace sp {
 namespace {
 
-template <int EPI>
-__device__ __forceinline__ const bf16* weight_row(const GemmParams& p, int tile_n0, int rho,
-                                                  int n_blk, int BN) {
-  if (EPI == kEpiSwiglu) {
-    const int pair = rho >> 5, w = rho & 31;
-    const int out = n_blk * (BN / 2) + 16 * pair + (w & 15);
-    return (const bf16*)(w < 16 ? p.b[0] : p.b[1]) + (int64_t)out * p.ldb;
-  }
-  const int n = tile_n0 + rho;
-  if (n < p.b_split0) return (const bf16*)p.b[0] + (int64_t)n * p.ldb;
-  if (n < p.b_split1) return (const bf16*)p.b[1] + (int64_t)(n - p.b_split0) * p.ldb;
-  return (const bf16*)p.b[2] + (int64_t)(n - p.b_split1) * p.ldb;
-}
-
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int BM, int BN, int EPI>
-__global__ __launch_bounds__(256) void gemm_mfma(const GemmParams p) {
-  constexpr int BK = 64, LD = BK + 8;
-  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
-  constexpr int AU = BM * 8 / 256, BU = BN * 8 / 256;  // 16-byte chunks per thread
-  static_assert(AU >= 1 && BU >= 1, "tile too small");
-  __shared__ __attribute__((aligned(16))) f16 As[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) f16 Bs[2][BN * LD];
+template <int BM, int BN, int WGM, int WGN, int S, int EPI>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
+  constexpr int NW = WGM * WGN, WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
+  constexpr int NIA = BM / 16, NI = NIA + BN / 16;  // 64-piece loads (16 rows each) per step
+  constexpr int IPW = (NI + NW - 1) / NW;            // loads per wave per step
+  constexpr int STAGE = (BM + BN) * 4;               // pieces per stage
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile");
+  static_assert(S >= 3 && (S - 2) * IPW < 64, "stages");
+  static_assert(EPI != kEpiSwiglu || WN % 32 == 0, "SwiGLU pairs 16 gate and 16 up columns");
+  __shared__ u32x4 lds[S * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, li = lane & 15, la = lane >> 4;
-  const int n_blk = blockIdx.x, m0 = blockIdx.y * BM, n0 = n_blk * BN;
-  const f16* A = (const f16*)p.a;
+  const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, la = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  __builtin_assume(wave >= 0 && wave < NW);
+  const int wm = wave / WGN, wn = wave % WGN;
 
-  const f16* arow[AU];
-  const bf16* brow[BU];
-  int aoff[AU], boff[BU];
-#pragma unroll
-  for (int u = 0; u < AU; ++u) {
-    const int q = tid + 256 * u, row = q >> 3;
-    const int gm = m0 + row < p.M ? m0 + row : p.M - 1;  // rows past M re-read row M-1; never stored
-    arow[u] = A + (int64_t)gm * p.lda + (q & 7) * 8;
-    aoff[u] = row * LD + (q & 7) * 8;
+  // Tile order: workgroups are dealt to the 8 XCDs round-robin, so the M tiles
+  // that share a weight tile get linear ids 8 apart (one XCD, one L2) and are
+  // dispatched together.
+  const int mtiles = (p.M + BM - 1) / BM, ntiles = p.N / BN;
+  const int L = blockIdx.x;
+  int m_tile, n_tile;
+  if ((ntiles & 7) == 0) {
+    const int r = L >> 3;
+    m_tile = r % mtiles;
+    n_tile = (r / mtiles) * 8 + (L & 7);
+  } else {
+    m_tile = L % mtiles;
+    n_tile = L / mtiles;
   }
-#pragma unroll
-  for (int u = 0; u < BU; ++u) {
-    const int q = tid + 256 * u, row = q >> 3;
-    brow[u] = weight_row<EPI>(p, n0, row, n_blk, BN) + (q & 7) * 8;
-    boff[u] = row * LD + (q & 7) * 8;
-  }
+  const int m0 = m_tile * BM, n0 = n_tile * BN;
 
-  uint4 ra[AU], rb[BU];
-  auto gload = [&](int kt) {
-    const int k0 = kt * BK;
+  // This wave's loads: slots j*NW + wave (mod NI; a wave count that does not
+  // divide NI re-issues a few slots with the same bytes).  Per slot: the
+  // 16-row block's base pointer (uniform), its place in the stage and the
+  // lane's byte offset (fixed; the K step adds 64 bytes to the base).
+  const char* gbase[IPW];
+  int lds_piece[IPW];
+  uint32_t lane_off[IPW];
+  const int row_in = lane >> 2, kp = (lane & 3) ^ (lane >> 4);
 #pragma unroll
-    for (int u = 0; u < AU; ++u) ra[u] = ld16(arow[u] + k0);
+  for (int j = 0; j < IPW; ++j) {
+    const int sl = (j * NW + wave) % NI;
+    if (sl < NIA) {
+      const int g = min(m0 + 16 * sl + row_in, p.M - 1);  // rows past M re-read row M-1; never stored
+      gbase[j] = (const char*)p.a;
+      lane_off[j] = (uint32_t)(g * p.lda * 2 + kp * 16);
+      lds_piece[j] = sl * 64;
+    } else {
+      const int rb = sl - NIA;  // 16-row block of the weight tile
+      int src, row;
+      if (EPI == kEpiSwiglu) {
+        src = rb & 1;
+        row = n_tile * (BN / 2) + 16 * (rb >> 1) + row_in;
+      } else {
+        const int n = n0 + 16 * rb;  // b_split0/1 are multiples of 16
+        src = n < p.b_split0 ? 0 : (n < p.b_split1 ? 1 : 2);
+        row = n - (src == 0 ? 0 : (src == 1 ? p.b_split0 : p.b_split1)) + row_in;
+      }
+      gbase[j] = (const char*)(src == 0 ? p.b[0] : (src == 1 ? p.b[1] : p.b[2]));
+      lane_off[j] = (uint32_t)(row * p.ldb * 2 + kp * 16);
+      lds_piece[j] = BM * 4 + rb * 64;
+    }
+  }
+  auto issue = [&](int kt, int stg) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < BU; ++u) rb[u] = bf16x8_to_f16x8(ld16(brow[u] + k0));
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < AU; ++u) st16(&As[buf][aoff[u]], ra[u]);
-#pragma unroll
-    for (int u = 0; u < BU; ++u) st16(&Bs[buf][boff[u]], rb[u]);
+    for (int j = 0; j < IPW; ++j)
+      ld16_to_lds<false>(gbase[j] + kt * 64, lane_off[j], &lds[stg * STAGE + lds_piece[j]]);
   };
 
   f32x4 acc[MT][NT];
@@ -83,30 +96,32 @@ __global__ __launch_bounds__(256) void gemm_mfma(const GemmParams p) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = p.K / BK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  // Steps past the last re-load the last one (into a stage no later step
+  // reads), so every step issues the same loads and one vmcnt value fits all.
+  const int KT = p.K / 32;
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st) issue(min(st, KT - 1), st);
+  int stg = 0;
   for (int kt = 0; kt < KT; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
+    wait_vmcnt<(S - 2) * IPW>();  // this wave's loads of step kt have landed
+    lds_barrier();                // everyone's have; everyone is done with step kt - 1
+    issue(min(kt + S - 1, KT - 1), stg == 0 ? S - 1 : stg - 1);
+    const u32x4* As = lds + stg * STAGE;
+    const u32x4* Bs = As + BM * 4;
+    const int sw = la ^ (li >> 2);  // swizzled piece of rows 16x + li
+    f16x8 af[MT], bfr[NT];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      f16x8 af[MT], bfr[NT];
+    for (int i = 0; i < MT; ++i) af[i] = __builtin_bit_cast(f16x8, As[(wm * WM + 16 * i + li) * 4 + sw]);
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-        af[i] = as_f16x8(ld16(&As[buf][(wm * WM + 16 * i + li) * LD + kk * 32 + 8 * la]));
+    for (int j = 0; j < NT; ++j)
+      bfr[j] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(Bs[(wn * WN + 16 * j + li) * 4 + sw]));
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
-        bfr[j] = as_f16x8(ld16(&Bs[buf][(wn * WN + 16 * j + li) * LD + kk * 32 + 8 * la]));
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
-    }
-    if (kt + 1 < KT) lstore(buf ^ 1);
-    __syncthreads();
+      for (int j = 0; j < NT; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+    stg = stg == S - 1 ? 0 : stg + 1;
   }
+  wait_vmcnt<0>();
 
   // Lane holds C[16i + 4la + r][16j + li] of the wave tile.
 #pragma unroll
@@ -119,7 +134,7 @@ __global__ __launch_bounds__(256) void gemm_mfma(const GemmParams p) {
 #pragma unroll
         for (int j = 0; j < NT; j += 2) {
           const int pair = (wn * WN + 16 * j) >> 5;
-          const int n = n_blk * (BN / 2) + 16 * pair + li;
+          const int n = n_tile * (BN / 2) + 16 * pair + li;
           const float gt = acc[i][j][r], up = acc[i][j + 1][r];
           ((f16*)p.c)[(int64_t)m * p.ldc + n] = (f16)(silu(gt) * up);
         }
@@ -171,22 +186,31 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }
 
-template <int BM, int BN>
-hipError_t launch_mfma_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
-  const dim3 grid(p.N / BN, (p.M + BM - 1) / BM);
+template <int BM, int BN, int WGM, int WGN, int S>
+hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
+  const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN)), block(64 * WGM * WGN);
   switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiStore>), grid, dim3(256), 0, s, p); break;
-    case kEpiResidRow: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiResidRow>), grid, dim3(256), 0, s, p); break;
-    case kEpiResidF32: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiResidF32>), grid, dim3(256), 0, s, p); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_mfma<BM, BN, kEpiSwiglu>), grid, dim3(256), 0, s, p); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiStore>), grid, block, 0, s, p); break;
+    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiResidRow>), grid, block, 0, s, p); break;
+    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiResidF32>), grid, block, 0, s, p); break;
+    case kEpiSwiglu:
+      if constexpr ((BN / WGN) % 32 == 0)
+        hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiSwiglu>), grid, block, 0, s, p);
+      else
+        return hipErrorInvalidValue;
+      break;
   }
   return hipGetLastError();
 }
 
-bool tile_ok(const GemmParams& p, Epilogue epi, int BN) {
-  if (p.N % BN) return false;
-  if (epi == kEpiSwiglu) return BN >= 64;
-  return p.b_split0 % BN == 0 && p.b_split1 % BN == 0;
+// Tile shapes: (BM, BN, waves along M, waves along N, stages).
+struct TileShape { int bm, bn, wgm, wgn; };
+constexpr TileShape kTiles[5] = {{128, 128, 2, 2}, {64, 128, 2, 2}, {32, 128, 1, 4}, {16, 64, 1, 2}, {16, 32, 1, 2}};
+
+bool tile_ok(const GemmParams& p, Epilogue epi, const TileShape& t) {
+  if (p.N % t.bn) return false;
+  if (epi == kEpiSwiglu) return (t.bn / t.wgn) % 32 == 0;
+  return p.b_split0 % t.bn == 0 && p.b_split1 % t.bn == 0;
 }
 
 }  // namespace
@@ -204,24 +228,23 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     }
     return hipGetLastError();
   }
-  if (p.K % 64) return hipErrorInvalidValue;
+  if (p.K % 32 || p.lda % 8 || p.ldb % 8) return hipErrorInvalidValue;
   // Largest tile that still gives one workgroup per compute unit (256), else the
   // tile with the most workgroups.
-  struct Cand { int bm, bn; };
-  const Cand cands[4] = {{128, 128}, {64, 128}, {32, 128}, {32, 64}};
   int best = -1;
   long best_tiles = -1;
-  for (int c = 0; c < 4; ++c) {
-    if (!tile_ok(p, epi, cands[c].bn)) continue;
-    const long tiles = (long)((p.M + cands[c].bm - 1) / cands[c].bm) * (p.N / cands[c].bn);
+  for (int c = 0; c < 5; ++c) {
+    if (!tile_ok(p, epi, kTiles[c])) continue;
+    const long tiles = (long)((p.M + kTiles[c].bm - 1) / kTiles[c].bm) * (p.N / kTiles[c].bn);
     if (tiles >= 256) { best = c; break; }
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
   switch (best) {
-    case 0: return launch_mfma_tile<128, 128>(epi, p, s);
-    case 1: return launch_mfma_tile<64, 128>(epi, p, s);
-    case 2: return launch_mfma_tile<32, 128>(epi, p, s);
-    case 3: return launch_mfma_tile<32, 64>(epi, p, s);
+    case 0: return launch_lds_tile<128, 128, 2, 2, 4>(epi, p, s);
+    case 1: return launch_lds_tile<64, 128, 2, 2, 6>(epi, p, s);
+    case 2: return launch_lds_tile<32, 128, 1, 4, 8>(epi, p, s);
+    case 3: return launch_lds_tile<16, 64, 1, 2, 8>(epi, p, s);
+    case 4: return launch_lds_tile<16, 32, 1, 2, 8>(epi, p, s);
   }
   return hipErrorInvalidValue;
 }
