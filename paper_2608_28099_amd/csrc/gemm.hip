@@ -3,13 +3,15 @@
 //
 // bf16 path: fp16 activations A, bf16 weights, v_mfma_f32_16x16x32_f16 with
 // fp32 accumulation.  A workgroup computes a BM x BN tile with WGM x WGN waves
-// (each a (BM/WGM) x (BN/WGN) sub-tile) and consumes K in steps of 32 (one MFMA
-// deep).  Each step's A and W tiles are loaded straight into LDS, S - 1 steps
-// ahead of use, through an S-stage ring (one barrier per step); weights stay
-// bf16 in LDS and are converted exactly to fp16 (|w| in [2^-14, 65504]) as a
-// wave reads its fragments.  A row of a stage tile is 32 values = four 16-byte
-// pieces; piece kp of row r sits at r * 4 + (kp ^ ((r >> 2) & 3)), so the 16
-// lanes that read piece kp of 16 consecutive rows hit 16 distinct bank groups.
+// (each a (BM/WGM) x (BN/WGN) sub-tile) and consumes K in steps of BK (32 or
+// 64: one or two MFMAs deep).  Each step's A and W tiles are loaded straight
+// into LDS, S - 1 steps ahead of use, through an S-stage ring (one barrier per
+// step); weights stay bf16 in LDS and are converted exactly to fp16 (|w| in
+// [2^-14, 65504]) as a wave reads its fragments.  A row of a stage tile is BK
+// values = PPR 16-byte pieces; piece kp of row r sits at
+//   r * PPR + (kp ^ ((r >> (4 - log2 PPR)) & (PPR - 1)))
+// so the 16 lanes that read piece kp of 16 consecutive rows hit 16 distinct
+// 16-byte bank groups.
 // SwiGLU: the BN weight rows of a tile alternate 16 gate rows and the 16
 // matching up rows, so every lane holds gate and up of the same outputs.
 #include "common.h"
@@ -20,12 +22,16 @@ namespace {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int BM, int BN, int WGM, int WGN, int S, int EPI>
+template <int BM, int BN, int WGM, int WGN, int S, int BK, int EPI>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   constexpr int NW = WGM * WGN, WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
-  constexpr int NIA = BM / 16, NI = NIA + BN / 16;  // 64-piece loads (16 rows each) per step
+  constexpr int PPR = BK / 8;                        // 16-byte pieces per tile row
+  constexpr int RPI = 64 / PPR;                      // tile rows per 64-piece load
+  constexpr int SWS = PPR == 4 ? 2 : 1;              // swizzle: kp ^ ((r >> SWS) & (PPR - 1))
+  constexpr int NIA = BM / RPI, NI = NIA + BN / RPI;  // 64-piece loads per step
   constexpr int IPW = (NI + NW - 1) / NW;            // loads per wave per step
-  constexpr int STAGE = (BM + BN) * 4;               // pieces per stage
+  constexpr int STAGE = (BM + BN) * PPR;             // pieces per stage
+  static_assert(BK == 32 || BK == 64, "step depth");
   static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile");
   static_assert(S >= 3 && (S - 2) * IPW < 64, "stages");
   static_assert(EPI != kEpiSwiglu || WN % 32 == 0, "SwiGLU pairs 16 gate and 16 up columns");
@@ -54,40 +60,42 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
 
   // This wave's loads: slots j*NW + wave (mod NI; a wave count that does not
   // divide NI re-issues a few slots with the same bytes).  Per slot: the
-  // 16-row block's base pointer (uniform), its place in the stage and the
-  // lane's byte offset (fixed; the K step adds 64 bytes to the base).
+  // RPI-row block's base pointer (uniform), its place in the stage and the
+  // lane's byte offset (fixed; each K step adds 2 BK bytes to the base).
   const char* gbase[IPW];
   int lds_piece[IPW];
   uint32_t lane_off[IPW];
-  const int row_in = lane >> 2, kp = (lane & 3) ^ (lane >> 4);
+  const int row_in = lane / PPR, kslot = lane % PPR;
 #pragma unroll
   for (int j = 0; j < IPW; ++j) {
     const int sl = (j * NW + wave) % NI;
+    const int blk = sl < NIA ? sl : sl - NIA;            // RPI-row block of the A or W tile
+    const int kp = kslot ^ (((blk * RPI + row_in) >> SWS) & (PPR - 1));
     if (sl < NIA) {
-      const int g = min(m0 + 16 * sl + row_in, p.M - 1);  // rows past M re-read row M-1; never stored
+      const int g = min(m0 + blk * RPI + row_in, p.M - 1);  // rows past M re-read row M-1; never stored
       gbase[j] = (const char*)p.a;
       lane_off[j] = (uint32_t)(g * p.lda * 2 + kp * 16);
-      lds_piece[j] = sl * 64;
+      lds_piece[j] = blk * 64;
     } else {
-      const int rb = sl - NIA;  // 16-row block of the weight tile
       int src, row;
-      if (EPI == kEpiSwiglu) {
-        src = rb & 1;
-        row = n_tile * (BN / 2) + 16 * (rb >> 1) + row_in;
+      if (EPI == kEpiSwiglu) {  // an RPI-row block lies inside one 16-row gate or up group
+        const int r = blk * RPI;
+        src = (r >> 4) & 1;
+        row = n_tile * (BN / 2) + 16 * (r >> 5) + (r & 15) + row_in;
       } else {
-        const int n = n0 + 16 * rb;  // b_split0/1 are multiples of 16
+        const int n = n0 + blk * RPI;  // b_split0/1 are multiples of BN
         src = n < p.b_split0 ? 0 : (n < p.b_split1 ? 1 : 2);
         row = n - (src == 0 ? 0 : (src == 1 ? p.b_split0 : p.b_split1)) + row_in;
       }
       gbase[j] = (const char*)(src == 0 ? p.b[0] : (src == 1 ? p.b[1] : p.b[2]));
       lane_off[j] = (uint32_t)(row * p.ldb * 2 + kp * 16);
-      lds_piece[j] = BM * 4 + rb * 64;
+      lds_piece[j] = BM * PPR + blk * 64;
     }
   }
   auto issue = [&](int kt, int stg) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < IPW; ++j)
-      ld16_to_lds<false>(gbase[j] + kt * 64, lane_off[j], &lds[stg * STAGE + lds_piece[j]]);
+      ld16_to_lds<false>(gbase[j] + kt * 2 * BK, lane_off[j], &lds[stg * STAGE + lds_piece[j]]);
   };
 
   f32x4 acc[MT][NT];
@@ -98,7 +106,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
 
   // Steps past the last re-load the last one (into a stage no later step
   // reads), so every step issues the same loads and one vmcnt value fits all.
-  const int KT = p.K / 32;
+  const int KT = p.K / BK;
 #pragma unroll
   for (int st = 0; st < S - 1; ++st) issue(min(st, KT - 1), st);
   int stg = 0;
@@ -107,18 +115,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
     lds_barrier();                // everyone's have; everyone is done with step kt - 1
     issue(min(kt + S - 1, KT - 1), stg == 0 ? S - 1 : stg - 1);
     const u32x4* As = lds + stg * STAGE;
-    const u32x4* Bs = As + BM * 4;
-    const int sw = la ^ (li >> 2);  // swizzled piece of rows 16x + li
-    f16x8 af[MT], bfr[NT];
+    const u32x4* Bs = As + BM * PPR;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) af[i] = __builtin_bit_cast(f16x8, As[(wm * WM + 16 * i + li) * 4 + sw]);
+    for (int ks = 0; ks < BK / 32; ++ks) {
+      // piece 4 ks + la of rows 16x + li (the row's swizzle depends on li only)
+      const int pc = (4 * ks + la) ^ ((li >> SWS) & (PPR - 1));
+      f16x8 af[MT], bfr[NT];
 #pragma unroll
-    for (int j = 0; j < NT; ++j)
-      bfr[j] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(Bs[(wn * WN + 16 * j + li) * 4 + sw]));
+      for (int i = 0; i < MT; ++i) af[i] = __builtin_bit_cast(f16x8, As[(wm * WM + 16 * i + li) * PPR + pc]);
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+      for (int j = 0; j < NT; ++j)
+        bfr[j] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(Bs[(wn * WN + 16 * j + li) * PPR + pc]));
 #pragma unroll
-      for (int j = 0; j < NT; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
+    }
     stg = stg == S - 1 ? 0 : stg + 1;
   }
   wait_vmcnt<0>();
@@ -186,16 +198,17 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }
 
-template <int BM, int BN, int WGM, int WGN, int S>
+template <int BM, int BN, int WGM, int WGN, int S, int BK>
 hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
+  if (p.K % BK) return hipErrorInvalidValue;
   const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN)), block(64 * WGM * WGN);
   switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiStore>), grid, block, 0, s, p); break;
-    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiResidRow>), grid, block, 0, s, p); break;
-    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiResidF32>), grid, block, 0, s, p); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore>), grid, block, 0, s, p); break;
+    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow>), grid, block, 0, s, p); break;
+    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32>), grid, block, 0, s, p); break;
     case kEpiSwiglu:
       if constexpr ((BN / WGN) % 32 == 0)
-        hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, kEpiSwiglu>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu>), grid, block, 0, s, p);
       else
         return hipErrorInvalidValue;
       break;
@@ -203,12 +216,16 @@ hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile shapes: (BM, BN, waves along M, waves along N, stages).
-struct TileShape { int bm, bn, wgm, wgn; };
-constexpr TileShape kTiles[5] = {{128, 128, 2, 2}, {64, 128, 2, 2}, {32, 128, 1, 4}, {16, 64, 1, 2}, {16, 32, 1, 2}};
+// Tile shapes, in order of preference (measured on the probe's projection
+// shapes): (BM, BN, waves along M, waves along N, stages, K-step depth).
+struct TileShape { int bm, bn, wgm, wgn, bk; };
+constexpr int kNumTiles = 7;
+constexpr TileShape kTiles[kNumTiles] = {{256, 192, 4, 2, 32}, {128, 64, 4, 2, 64}, {64, 64, 2, 2, 64},
+                                         {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64}, {16, 16, 1, 1, 64},
+                                         {16, 32, 1, 1, 32}};
 
 bool tile_ok(const GemmParams& p, Epilogue epi, const TileShape& t) {
-  if (p.N % t.bn) return false;
+  if (p.N % t.bn || p.K % t.bk) return false;
   if (epi == kEpiSwiglu) return (t.bn / t.wgn) % 32 == 0;
   return p.b_split0 % t.bn == 0 && p.b_split1 % t.bn == 0;
 }
@@ -229,22 +246,24 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     return hipGetLastError();
   }
   if (p.K % 32 || p.lda % 8 || p.ldb % 8) return hipErrorInvalidValue;
-  // Largest tile that still gives one workgroup per compute unit (256), else the
-  // tile with the most workgroups.
+  // First tile (in preference order) that gives at least one workgroup per
+  // compute unit (256), else the valid tile with the most workgroups.
   int best = -1;
   long best_tiles = -1;
-  for (int c = 0; c < 5; ++c) {
+  for (int c = 0; c < kNumTiles; ++c) {
     if (!tile_ok(p, epi, kTiles[c])) continue;
     const long tiles = (long)((p.M + kTiles[c].bm - 1) / kTiles[c].bm) * (p.N / kTiles[c].bn);
     if (tiles >= 256) { best = c; break; }
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
   switch (best) {
-    case 0: return launch_lds_tile<128, 128, 2, 2, 4>(epi, p, s);
-    case 1: return launch_lds_tile<64, 128, 2, 2, 6>(epi, p, s);
-    case 2: return launch_lds_tile<32, 128, 1, 4, 8>(epi, p, s);
-    case 3: return launch_lds_tile<16, 64, 1, 2, 8>(epi, p, s);
-    case 4: return launch_lds_tile<16, 32, 1, 2, 8>(epi, p, s);
+    case 0: return launch_lds_tile<256, 192, 4, 2, 3, 32>(epi, p, s);
+    case 1: return launch_lds_tile<128, 64, 4, 2, 6, 64>(epi, p, s);
+    case 2: return launch_lds_tile<64, 64, 2, 2, 8, 64>(epi, p, s);
+    case 3: return launch_lds_tile<32, 64, 1, 2, 8, 64>(epi, p, s);
+    case 4: return launch_lds_tile<16, 32, 1, 1, 8, 64>(epi, p, s);
+    case 5: return launch_lds_tile<16, 16, 1, 1, 8, 64>(epi, p, s);
+    case 6: return launch_lds_tile<16, 32, 1, 1, 8, 32>(epi, p, s);
   }
   return hipErrorInvalidValue;
 }
