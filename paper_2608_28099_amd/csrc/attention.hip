@@ -1,14 +1,15 @@
-// Split attention of the k soft queries over the cached prefix plus the soft
-// keys (Sec. 3.3 Eq. 1-3), and the merge of the splits.
+// Split attention of the k soft queries over the cached prefix (Sec. 3.3,
+// Eq. 1-3), and the merge of the splits with the soft keys themselves.
 //
-// Work unit: one wave per (sequence b, KV head g, query group, split s).  The
-// rows of a KV head are its k*G soft queries (row r = j*G + h%G for soft row j
-// and query head h = g*G + h%G); a query group is 16*QT consecutive rows.
-// Split s covers cache tokens [s*split_len, min(N_b, (s+1)*split_len)); split 0
-// also covers the soft keys.  Each wave keeps an online softmax (running max m
-// in log2 units, running sum l, unnormalised output O) and writes them as a
-// partial; the merge combines partials with the log-sum-exp rule
-//   M = max_s m_s,  L = sum_s l_s 2^(m_s - M),  O = sum_s O_s 2^(m_s - M) / L.
+// Rows of a KV head: its k*G soft queries (row r = j*G + h%G for soft row j and
+// query head h = g*G + h%G).  Split s covers cache tokens [s*split_len,
+// min(N_b, (s+1)*split_len)).  Each split keeps an online softmax per row
+// (running max m in log2 units, running sum l, unnormalised output O) and
+// writes it as a partial.  The merge computes, per row, the soft keys visible
+// to it (causal: key j' <= j) in fp32 and combines everything with the
+// log-sum-exp rule
+//   M = max(m_soft, max_s m_s),  L = l_soft 2^(m_soft-M) + sum_s l_s 2^(m_s-M),
+//   O = (O_soft 2^(m_soft-M) + sum_s O_s 2^(m_s-M)) / L.
 //
 // bf16 path: bf16 KV cache, bf16 MFMA operands, fp32 accumulation.  The two
 // operands the kernel itself rounds, the queries and the probabilities, are
@@ -17,17 +18,15 @@
 // One workgroup per (sequence, KV head, query group, split) with one wave per
 // 16-row query tile.  The split's tokens are consumed in units of 32 (two
 // 16-token halves, each inside one block):
-//   * all lanes of the workgroup fetch the unit's K and V tiles with 16-byte
-//     streaming loads (1 KB contiguous per wave instruction), two units ahead,
-//     and copy them into one of two LDS stages (in a tail unit, slots past the
-//     end are zeroed on the way: their bytes may be anything, NaN included);
+//   * the workgroup loads each unit's K and V tiles straight into LDS (16-byte
+//     direct loads, streaming), two units ahead, through three LDS stages; in
+//     a tail unit, V slots past the end are zeroed after landing (their bytes
+//     may be anything, NaN included);
 //   * every wave reads its fragments from LDS and runs its query tile:
-//     S^T = K Q^T on v_mfma_f32_16x16x32_bf16 with a half's 16 tokens as MFMA
-//     rows, so lane (li, la) ends up with tokens 4la..4la+3 of both halves for
-//     query li: 8 values = the A operand of v_mfma_f32_16x16x32_bf16 for
-//     O += P V (k-slot 4h + r stands for token 16h + 4la + r); P never goes
-//     through LDS; the B operand is V[those 8 tokens][16nt + li], which the
-//     staging has placed in 16 contiguous bytes (one conflict-free LDS read).
+//     S^T = K Q^T on v_mfma_f32_16x16x32_bf16, so that lane (li, la) ends up
+//     with 8 consecutive tokens of query li: the A operand of
+//     v_mfma_f32_16x16x32_bf16 for O += P V (P never goes through LDS); the B
+//     operand is V[those 8 tokens][16nt + li], 16 contiguous LDS bytes.
 // Online softmax in log2 units with a lazy reference max (see kRescaleLog2).
 #include "common.h"
 #include "kernels.h"
@@ -62,12 +61,10 @@ struct RowState {
 // One 32-token unit for one wave, in two phases.  qk_unit: kf[h][c] =
 // K[token pi_h(li)][8 (la*NC + c) ..] (the unit layout below); score i of the
 // lane (i = 4h + r) is token 8la + i for query li.  softmax_pv_unit: vf[nt] =
-// V[tokens 8la..8la+7][16nt + li].  SOFT: the soft keys, whose K and V are
-// themselves hi + lo pairs (kl, vl) and whose visibility is causal; cache units
-// mask keys at or past `limit`.
-template <int HD, bool SOFT>
+// V[tokens 8la..8la+7][16nt + li]; keys at or past `limit` are masked.
+template <int HD>
 __device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
-                                        const bf16x8 (&kl)[2][HD / 32], f32x4& s0, f32x4& s1) {
+                                        f32x4& s0, f32x4& s1) {
   constexpr int NC = HD / 32;
   s0 = f32x4{0.f, 0.f, 0.f, 0.f};
   s1 = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -77,28 +74,15 @@ __device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&k
     s1 = mfma16x16x32_bf16(kf[1][c], st.qh[c], s1);
     s0 = mfma16x16x32_bf16(kf[0][c], st.ql[c], s0);
     s1 = mfma16x16x32_bf16(kf[1][c], st.ql[c], s1);
-    if (SOFT) {
-      s0 = mfma16x16x32_bf16(kl[0][c], st.qh[c], s0);
-      s1 = mfma16x16x32_bf16(kl[1][c], st.qh[c], s1);
-    }
   }
 }
 
-template <int HD, bool SOFT>
+template <int HD>
 __device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x4 s1,
-                                                const bf16x8 (&vf)[HD / 16],
-                                                const bf16x8 (&vl)[HD / 16], int li, int la,
-                                                int limit, int key0, int row, int group, int k) {
+                                                const bf16x8 (&vf)[HD / 16], int la, int limit) {
   constexpr int NT = HD / 16;
   float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
-  if (SOFT) {
-    // soft key j' is visible to query row r iff j' <= r / G (causal, own row included)
-    int jmax = row / group;
-    jmax = jmax < k - 1 ? jmax : k - 1;
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (key0 + 8 * la + i > jmax) sc[i] = -INFINITY;
-  } else if (limit < 32) {
+  if (limit < 32) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
       if (8 * la + i >= limit) sc[i] = -INFINITY;
@@ -139,7 +123,6 @@ __device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x
   for (int nt = 0; nt < NT; ++nt) {
     st.o[nt] = mfma16x16x32_bf16(ph, vf[nt], st.o[nt]);
     st.o[nt] = mfma16x16x32_bf16(pl, vf[nt], st.o[nt]);
-    if (SOFT) st.o[nt] = mfma16x16x32_bf16(ph, vl[nt], st.o[nt]);
   }
 }
 
@@ -203,7 +186,7 @@ __device__ __forceinline__ void zero_tail(u32x4* sb, int limit, int tid) {
 // A wave's fragments of a staged unit, then the unit's softmax and products.
 template <int HD>
 __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, int limit, int li,
-                                             int la, int row) {
+                                             int la) {
   constexpr int NC = HD / 32, NT = HD / 16;
   f32x4 s0, s1;
   {
@@ -213,7 +196,7 @@ __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, 
 #pragma unroll
       for (int c = 0; c < NC; ++c)
         kf[h][c] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::k_piece(h, la * NC + c, li)]);
-    qk_unit<HD, false>(st, kf, kf, s0, s1);
+    qk_unit<HD>(st, kf, s0, s1);
   }
   // V fragments are read only once the QK products are issued, into the
   // registers the K fragments held.
@@ -222,7 +205,7 @@ __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, 
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
     vf[nt] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::v_piece(nt, li, la)]);
-  softmax_pv_unit<HD, false>(st, s0, s1, vf, vf, li, la, limit, 0, row, 1, 1);
+  softmax_pv_unit<HD>(st, s0, s1, vf, la, limit);
 }
 
 // W waves per workgroup, one per 16-row query tile.  Three LDS stages: unit u
@@ -263,40 +246,6 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     for (int nt = 0; nt < NT; ++nt) st.o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     st.m = kNegBig;
     st.l = 0.f;
-  }
-
-  if (s == 0) {
-    // the soft keys: hi/lo bf16 tiles of ks tokens (a multiple of 32), read in
-    // place with the unit's token order
-    const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * HD, vo = (int64_t)g * HD * p.ks;
-    const bf16 *kt = (const bf16*)p.k_soft + ko, *ktl = (const bf16*)p.k_soft_lo + ko;
-    const bf16 *vt = (const bf16*)p.v_soft + vo, *vtl = (const bf16*)p.v_soft_lo + vo;
-    for (int c0 = 0; c0 < p.k; c0 += 32) {
-      f32x4 s0, s1;
-      {
-        bf16x8 kf[2][NC], kl[2][NC];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int tk = c0 + 8 * (li >> 2) + 4 * h + (li & 3);
-#pragma unroll
-          for (int c = 0; c < NC; ++c) {
-            const int64_t e = ((int64_t)(la * NC + c) * p.ks + tk) * 8;
-            kf[h][c] = __builtin_bit_cast(bf16x8, ld16v(kt + e));
-            kl[h][c] = __builtin_bit_cast(bf16x8, ld16v(ktl + e));
-          }
-        }
-        qk_unit<HD, true>(st, kf, kl, s0, s1);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      bf16x8 vf[NT], vl[NT];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int64_t e = (int64_t)(16 * nt + li) * p.ks + c0 + 8 * la;
-        vf[nt] = __builtin_bit_cast(bf16x8, ld16v(vt + e));
-        vl[nt] = __builtin_bit_cast(bf16x8, ld16v(vtl + e));
-      }
-      softmax_pv_unit<HD, true>(st, s0, s1, vf, vl, li, la, 32, c0, row0 + li, p.group, p.k);
-    }
   }
 
   const int nunits = (t1 - t0 + 31) >> 5;   // 0 when the split has no cache tokens
@@ -371,7 +320,7 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
         lds_barrier();
       }
       if (u + 2 <= last) issue(u + 2, buf == 0 ? 2 : buf - 1);
-      compute_unit<HD>(st, stage[buf], limit, li, la, row0 + li);
+      compute_unit<HD>(st, stage[buf], limit, li, la);
       buf = buf == 2 ? 0 : buf + 1;
     }
   }
@@ -420,19 +369,12 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
   for (int u = 0; u < OPT; ++u) oacc[u] = 0.f;
   __syncthreads();
 
-  // is_soft: chunk of soft keys starting at key c0; else cache tokens [c0, c0 + TT).
-  auto run_chunk = [&](bool is_soft, int c0) {
+  // cache tokens [c0, c0 + TT)
+  auto run_chunk = [&](int c0) {
     for (int idx = tid; idx < TT * HD; idx += 256) {
       const int t = idx / HD, i = idx % HD, tok = c0 + t;
       float kv = 0.f, vv = 0.f;
-      if (is_soft) {
-        if (tok < p.k) {
-          const float* kt = (const float*)p.k_soft + ((int64_t)b * p.n_kv + g) * p.ks * HD;
-          const float* vt = (const float*)p.v_soft + (int64_t)g * HD * p.ks;
-          kv = kt[((int64_t)(i / X) * p.ks + tok) * X + i % X];
-          vv = vt[(int64_t)i * p.ks + tok];
-        }
-      } else if (tok < t1) {
+      if (tok < t1) {
         const int64_t blk = phys_block(p, b, tok);
         const int slot = tok & (bs - 1);
         const float* kt = (const float*)p.k_base + blk * p.k_sb + (int64_t)g * p.k_sh;
@@ -445,18 +387,10 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
     }
     __syncthreads();
     for (int idx = tid; idx < R * TT; idx += 256) {
-      const int r = idx / TT, t = idx % TT, tok = c0 + t;
+      const int r = idx / TT, t = idx % TT;
       float acc = 0.f;
       for (int i = 0; i < HD; ++i) acc += qs[r][i] * ks[t][i];
-      bool ok;
-      if (is_soft) {
-        int jmax = r / p.group;
-        jmax = jmax < p.k - 1 ? jmax : p.k - 1;
-        ok = tok <= jmax;
-      } else {
-        ok = tok < t1;
-      }
-      ps[r][t] = ok ? acc : -INFINITY;
+      ps[r][t] = c0 + t < t1 ? acc : -INFINITY;
     }
     __syncthreads();
     if (tid < R) {
@@ -487,9 +421,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
     __syncthreads();
   };
 
-  if (s == 0)
-    for (int c0 = 0; c0 < p.k; c0 += TT) run_chunk(true, c0);
-  for (int c0 = t0; c0 < t1; c0 += TT) run_chunk(false, c0);
+  for (int c0 = t0; c0 < t1; c0 += TT) run_chunk(c0);
 
   const int64_t prow = (((int64_t)b * p.n_kv + g) * p.max_splits + s) * p.r_alloc;
   if (tid < R) p.ml_part[prow + tid] = make_float2(m_s[tid], l_s[tid]);
@@ -503,8 +435,20 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
 
 // ---------------------------------------------------------------- merge
 // One wave per row (b, g, r); lanes cover the head dimension.
-template <typename T>
+// Soft-key operands as stored by rope_scatter: fp32, or bf16 hi + lo parts.
+template <typename TI>
+__device__ __forceinline__ float soft_at(const void* hi, const void* lo, int64_t idx) {
+  if constexpr (sizeof(TI) == 4) return ((const float*)hi)[idx];
+  else return (float)((const bf16*)hi)[idx] + (float)((const bf16*)lo)[idx];
+}
+
+// One wave per (sequence b, KV head g, row r): the soft keys visible to the row
+// (j' <= j = r / G, in fp32 from the stored operands; lane = key), then the
+// log-sum-exp combination with the split partials; lanes over head dims.
+// TO: output (activation) type; TI: storage of the soft operands.
+template <typename TO, typename TI>
 __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
+  constexpr int X = 16 / sizeof(TI);  // chunk width of the soft-key tile
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave, g = blockIdx.y, b = blockIdx.z;
   if (r >= p.rows) return;
@@ -512,23 +456,42 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
   const int64_t base = ((int64_t)b * p.n_kv + g) * p.max_splits * p.r_alloc + r;
-  float M = kNegBig;
+  const int j = r / p.group, h = g * p.group + r % p.group;
+
+  // soft scores (log2 units; q carries log2(e)/sqrt(hd)), key j' = lane
+  float sc = -INFINITY;
+  if (lane <= j) {
+    const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + r) * p.hd;
+    const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * p.hd;
+    float acc = 0.f;
+    for (int i = 0; i < p.hd; ++i)
+      acc += soft_at<TI>(p.q, p.q_lo, qo + i) *
+             soft_at<TI>(p.k_soft, p.k_soft_lo, ko + ((int64_t)(i / X) * p.ks + lane) * X + i % X);
+    sc = acc;
+  }
+  float ms = sc;
+  for (int o = 32; o > 0; o >>= 1) ms = fmaxf(ms, __shfl_xor(ms, o));
+  float M = ms;  // j >= 0, so key 0 is always visible: finite
   for (int s = 0; s < ns; ++s) M = fmaxf(M, p.ml_part[base + (int64_t)s * p.r_alloc].x);
-  float L = 0.f;
+  const float pj = lane <= j ? fast_exp2(sc - M) : 0.f;
+  float L = pj;
+  for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
   for (int s = 0; s < ns; ++s) {
     const float2 ml = p.ml_part[base + (int64_t)s * p.r_alloc];
     L += ml.y * fast_exp2(ml.x - M);
   }
   const float inv = 1.0f / L;
-  const int j = r / p.group, h = g * p.group + r % p.group;
-  T* out = (T*)p.out + ((int64_t)b * p.k + j) * ((int64_t)p.n_q * p.hd) + (int64_t)h * p.hd;
-  for (int i = lane; i < p.hd; i += 64) {
+  TO* out = (TO*)p.out + ((int64_t)b * p.k + j) * ((int64_t)p.n_q * p.hd) + (int64_t)h * p.hd;
+  const int64_t vo = (int64_t)g * p.hd * p.ks;
+  for (int i0 = 0; i0 < p.hd; i0 += 64) {
+    const int i = i0 + lane;  // hd is 64 or 128
     float acc = 0.f;
     for (int s = 0; s < ns; ++s) {
       const int64_t row = base + (int64_t)s * p.r_alloc;
       acc += p.o_part[row * p.hd + i] * fast_exp2(p.ml_part[row].x - M);
     }
-    out[i] = from_f32<T>(acc * inv);
+    for (int jj = 0; jj <= j; ++jj) acc += __shfl(pj, jj) * soft_at<TI>(p.v_soft, p.v_soft_lo, vo + (int64_t)i * p.ks + jj);
+    out[i] = from_f32<TO>(acc * inv);
   }
 }
 
@@ -564,10 +527,11 @@ hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStrea
 
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s) {
   const dim3 grid((p.rows + 3) / 4, p.n_kv, batch);
+  if (p.hd != 64 && p.hd != 128) return hipErrorInvalidValue;
   if (dt == kBF16)  // the attention output feeds an fp16 MFMA
-    hipLaunchKernelGGL(merge_splits<f16>, grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((merge_splits<f16, bf16>), grid, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(merge_splits<float>, grid, dim3(256), 0, s, p);
+    hipLaunchKernelGGL((merge_splits<float, float>), grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

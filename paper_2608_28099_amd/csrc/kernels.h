@@ -37,11 +37,7 @@ hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStre
 // ---------------------------------------------------------------- attention
 struct AttnParams {
   const void* q;           // [B][n_kv][r_alloc][hd], pre-scaled by log2(e)/sqrt(hd)
-  const void* k_soft;      // [B][n_kv] chunked tiles of ks tokens
-  const void* v_soft;      // [n_kv][hd][ks]
-  const void* q_lo;        // bf16 path: remainders of q, k_soft, v_soft (same layouts)
-  const void* k_soft_lo;
-  const void* v_soft_lo;
+  const void* q_lo;        // bf16 path: remainders of q (same layout)
   const void* k_base;
   const void* v_base;
   int64_t k_sb, k_sh, v_sb, v_sh;     // elements
@@ -50,11 +46,12 @@ struct AttnParams {
   const int* err;          // nullable
   float* o_part;           // [B][n_kv][max_splits][r_alloc][hd] fp32, unnormalised
   float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
-  int n_kv, group, k, rows, r_alloc, ks, n_qgroups;
+  int n_kv, rows, r_alloc, n_qgroups;
   int bs_log2, mbps, max_seq_len, split_len, max_splits;
 };
+// Cache tokens only (the soft keys are folded in by the merge).
 // bf16-storage path (bf16 MFMA, split Q and P): head_dim 64/128, `waves` 16-row
-// query tiles per workgroup (1, 2, 3, 4, 5, 6, 8, 10, 12 or 16).
+// query tiles per workgroup (1, 2, 3, 4, 5, 6 or 8; up to 16 for head_dim 64).
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s);
 // fp32 VALU path: head_dim 64/128, rows <= 64.
 hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);
@@ -64,8 +61,15 @@ struct MergeParams {
   const float2* ml_part;
   const int* seq_lens;
   const int* err;
+  // the soft keys, in the layouts rope_scatter writes (bf16 path: hi and lo parts)
+  const void* q;
+  const void* q_lo;
+  const void* k_soft;
+  const void* k_soft_lo;
+  const void* v_soft;
+  const void* v_soft_lo;
   void* out;               // [B k][n_q hd] (activation dtype)
-  int n_kv, group, k, rows, r_alloc, hd, max_splits, split_len, max_seq_len, n_q;
+  int n_kv, group, k, rows, r_alloc, hd, ks, max_splits, split_len, max_seq_len, n_q;
 };
 // dt: storage dtype of the config (the output is fp16 for bf16 storage)
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s);

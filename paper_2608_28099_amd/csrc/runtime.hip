@@ -308,11 +308,7 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   // stage 1: split attention over [cached K/V ; soft K/V]
   AttnParams ap{};
   ap.q = at<void>(h, pl.off_q);
-  ap.k_soft = at<void>(h, pl.off_ksoft);
-  ap.v_soft = at<void>(h, pl.off_vsoft);
   ap.q_lo = at<void>(h, pl.off_q_lo);
-  ap.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
-  ap.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
   ap.k_base = kv->k_base; ap.v_base = kv->v_base;
   ap.k_sb = kv->k_stride_block; ap.k_sh = kv->k_stride_head;
   ap.v_sb = kv->v_stride_block; ap.v_sh = kv->v_stride_head;
@@ -321,8 +317,8 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   ap.err = errp;
   ap.o_part = at<float>(h, pl.off_opart);
   ap.ml_part = at<float2>(h, pl.off_ml);
-  ap.n_kv = c.n_kv_heads; ap.group = pl.group; ap.k = c.k; ap.rows = pl.rows;
-  ap.r_alloc = pl.r_alloc; ap.ks = pl.ks; ap.n_qgroups = pl.n_qgroups;
+  ap.n_kv = c.n_kv_heads; ap.rows = pl.rows;
+  ap.r_alloc = pl.r_alloc; ap.n_qgroups = pl.n_qgroups;
   ap.bs_log2 = ilog2(kv->block_size); ap.mbps = kv->max_blocks_per_seq;
   ap.max_seq_len = c.max_seq_len; ap.split_len = pl.split_len; ap.max_splits = pl.max_splits;
   if (dt == kBF16)
@@ -335,9 +331,12 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   {
     MergeParams mp{};
     mp.o_part = ap.o_part; mp.ml_part = ap.ml_part; mp.seq_lens = seq_lens; mp.err = errp;
+    mp.q = ap.q; mp.q_lo = ap.q_lo;
+    mp.k_soft = at<void>(h, pl.off_ksoft); mp.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
+    mp.v_soft = at<void>(h, pl.off_vsoft); mp.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
     mp.out = at<void>(h, pl.off_attn);
     mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.k = c.k; mp.rows = pl.rows;
-    mp.r_alloc = pl.r_alloc; mp.hd = hd; mp.max_splits = pl.max_splits;
+    mp.r_alloc = pl.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = pl.max_splits;
     mp.split_len = pl.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
     SP_TRY(launch_merge(dt, mp, B, s));
   }
