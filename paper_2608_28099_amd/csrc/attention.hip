@@ -435,20 +435,27 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
 
 // ---------------------------------------------------------------- merge
 // One wave per row (b, g, r); lanes cover the head dimension.
-// Soft-key operands as stored by rope_scatter: fp32, or bf16 hi + lo parts.
-template <typename TI>
-__device__ __forceinline__ float soft_at(const void* hi, const void* lo, int64_t idx) {
-  if constexpr (sizeof(TI) == 4) return ((const float*)hi)[idx];
-  else return (float)((const bf16*)hi)[idx] + (float)((const bf16*)lo)[idx];
+// DPL consecutive soft operands as stored by rope_scatter: fp32, or bf16 hi + lo parts.
+template <typename TI, int DPL>
+__device__ __forceinline__ void soft_load(const void* hi, const void* lo, int64_t idx, float (&v)[DPL]) {
+  if constexpr (sizeof(TI) == 4) {
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) v[d] = ((const float*)hi)[idx + d];
+  } else {
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) v[d] = (float)((const bf16*)hi)[idx + d] + (float)((const bf16*)lo)[idx + d];
+  }
 }
 
-// One wave per (sequence b, KV head g, row r): the soft keys visible to the row
-// (j' <= j = r / G, in fp32 from the stored operands; lane = key), then the
-// log-sum-exp combination with the split partials; lanes over head dims.
-// TO: output (activation) type; TI: storage of the soft operands.
-template <typename TO, typename TI>
+// One wave per (sequence b, KV head g, row r); lane l owns head dims
+// l * DPL .. l * DPL + DPL - 1 (DPL = hd / 64).  The soft keys visible to the
+// row (j' <= j = r / G) are scored in fp32 from the stored operands (lane
+// partial + wave reduction per key), then the split partials are folded in
+// with a running maximum (log-sum-exp rule), four at a time so that their
+// loads are in flight together.  TO: output type; TI: soft operand storage.
+template <typename TO, typename TI, int DPL>
 __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
-  constexpr int X = 16 / sizeof(TI);  // chunk width of the soft-key tile
+  constexpr int C = 4;  // keys / splits per batch of loads
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave, g = blockIdx.y, b = blockIdx.z;
   if (r >= p.rows) return;
@@ -457,42 +464,83 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
   const int64_t base = ((int64_t)b * p.n_kv + g) * p.max_splits * p.r_alloc + r;
   const int j = r / p.group, h = g * p.group + r % p.group;
+  const int i0 = lane * DPL;
 
-  // soft scores (log2 units; q carries log2(e)/sqrt(hd)), key j' = lane
-  float sc = -INFINITY;
-  if (lane <= j) {
-    const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + r) * p.hd;
-    const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * p.hd;
-    float acc = 0.f;
-    for (int i = 0; i < p.hd; ++i)
-      acc += soft_at<TI>(p.q, p.q_lo, qo + i) *
-             soft_at<TI>(p.k_soft, p.k_soft_lo, ko + ((int64_t)(i / X) * p.ks + lane) * X + i % X);
-    sc = acc;
+  const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + r) * p.hd + i0;
+  const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * p.hd + i0;  // [ks][hd]
+  const int64_t vo = (int64_t)g * p.ks * p.hd + i0;                 // [ks][hd]
+  float qv[DPL];
+  soft_load<TI, DPL>(p.q, p.q_lo, qo, qv);
+  // soft scores in log2 units (q carries log2(e)/sqrt(hd)); lane jj keeps key jj's.
+  // Slots past j (up to the tile width ks, a multiple of 32) are read but unused.
+  float my = -INFINITY;
+  for (int j0 = 0; j0 <= j; j0 += C) {
+    float kv[C][DPL];
+#pragma unroll
+    for (int c = 0; c < C; ++c) soft_load<TI, DPL>(p.k_soft, p.k_soft_lo, ko + (int64_t)(j0 + c) * p.hd, kv[c]);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      float part = 0.f;
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) part += qv[d] * kv[c][d];
+      for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o);
+      if (lane == j0 + c && j0 + c <= j) my = part;
+    }
   }
-  float ms = sc;
-  for (int o = 32; o > 0; o >>= 1) ms = fmaxf(ms, __shfl_xor(ms, o));
-  float M = ms;  // j >= 0, so key 0 is always visible: finite
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, p.ml_part[base + (int64_t)s * p.r_alloc].x);
-  const float pj = lane <= j ? fast_exp2(sc - M) : 0.f;
+  float M = my;  // key 0 is always visible: finite
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+  const float pj = lane <= j ? fast_exp2(my - M) : 0.f;
   float L = pj;
   for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
-  for (int s = 0; s < ns; ++s) {
-    const float2 ml = p.ml_part[base + (int64_t)s * p.r_alloc];
-    L += ml.y * fast_exp2(ml.x - M);
+  float acc[DPL];
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) acc[d] = 0.f;
+  for (int j0 = 0; j0 <= j; j0 += C) {
+    float vv[C][DPL];
+#pragma unroll
+    for (int c = 0; c < C; ++c) soft_load<TI, DPL>(p.v_soft, p.v_soft_lo, vo + (int64_t)(j0 + c) * p.hd, vv[c]);
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const float pk = __shfl(pj, j0 + c);
+      if (j0 + c <= j)  // slots past j may hold anything, NaN included
+#pragma unroll
+        for (int d = 0; d < DPL; ++d) acc[d] += pk * vv[c][d];
+    }
+  }
+  // split partials, folded in with a running maximum
+  for (int s0 = 0; s0 < ns; s0 += C) {
+    float2 ml[C];
+    float ov[C][DPL];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      const int64_t row = base + (int64_t)min(s0 + c, ns - 1) * p.r_alloc;
+      ml[c] = p.ml_part[row];
+#pragma unroll
+      for (int d = 0; d < DPL; ++d) ov[c][d] = p.o_part[row * p.hd + i0 + d];
+    }
+    float mn = M;
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+      if (s0 + c < ns) mn = fmaxf(mn, ml[c].x);
+    const float alpha = fast_exp2(M - mn);
+    L *= alpha;
+#pragma unroll
+    for (int d = 0; d < DPL; ++d) acc[d] *= alpha;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+      if (s0 + c < ns) {
+        const float wgt = fast_exp2(ml[c].x - mn);
+        L += ml[c].y * wgt;
+#pragma unroll
+        for (int d = 0; d < DPL; ++d) acc[d] += ov[c][d] * wgt;
+      }
+    }
+    M = mn;
   }
   const float inv = 1.0f / L;
-  TO* out = (TO*)p.out + ((int64_t)b * p.k + j) * ((int64_t)p.n_q * p.hd) + (int64_t)h * p.hd;
-  const int64_t vo = (int64_t)g * p.hd * p.ks;
-  for (int i0 = 0; i0 < p.hd; i0 += 64) {
-    const int i = i0 + lane;  // hd is 64 or 128
-    float acc = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const int64_t row = base + (int64_t)s * p.r_alloc;
-      acc += p.o_part[row * p.hd + i] * fast_exp2(p.ml_part[row].x - M);
-    }
-    for (int jj = 0; jj <= j; ++jj) acc += __shfl(pj, jj) * soft_at<TI>(p.v_soft, p.v_soft_lo, vo + (int64_t)i * p.ks + jj);
-    out[i] = from_f32<TO>(acc * inv);
-  }
+  TO* out = (TO*)p.out + ((int64_t)b * p.k + j) * ((int64_t)p.n_q * p.hd) + (int64_t)h * p.hd + i0;
+#pragma unroll
+  for (int d = 0; d < DPL; ++d) out[d] = from_f32<TO>(acc[d] * inv);
 }
 
 }  // namespace
@@ -528,10 +576,13 @@ hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStrea
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s) {
   const dim3 grid((p.rows + 3) / 4, p.n_kv, batch);
   if (p.hd != 64 && p.hd != 128) return hipErrorInvalidValue;
-  if (dt == kBF16)  // the attention output feeds an fp16 MFMA
-    hipLaunchKernelGGL((merge_splits<f16, bf16>), grid, dim3(256), 0, s, p);
-  else
-    hipLaunchKernelGGL((merge_splits<float, float>), grid, dim3(256), 0, s, p);
+  if (dt == kBF16) {  // the attention output feeds an fp16 MFMA
+    if (p.hd == 128) hipLaunchKernelGGL((merge_splits<f16, bf16, 2>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((merge_splits<f16, bf16, 1>), grid, dim3(256), 0, s, p);
+  } else {
+    if (p.hd == 128) hipLaunchKernelGGL((merge_splits<float, float, 2>), grid, dim3(256), 0, s, p);
+    else hipLaunchKernelGGL((merge_splits<float, float, 1>), grid, dim3(256), 0, s, p);
+  }
   return hipGetLastError();
 }
 

@@ -20,8 +20,8 @@ struct RopeParams {
   const int* seq_lens;     // device [B]
   const int* err;          // nullable: skip everything if *err != 0
   void* q;                 // [B][n_kv][r_alloc][hd], scaled by q_scale
-  void* k_soft;            // [B][n_kv] tiles of ks tokens, chunked layout (x = 16 B / elem)
-  void* v_soft;            // [n_kv][hd][ks] (batch-invariant)
+  void* k_soft;            // [B][n_kv][ks][hd] (rotated soft keys)
+  void* v_soft;            // [n_kv][ks][hd] (batch-invariant)
   // bf16 split output (dt == kBF16): q, k_soft, v_soft receive bf16(x) and these
   // the remainders bf16(x - bf16(x)), same layouts
   void* q_lo;

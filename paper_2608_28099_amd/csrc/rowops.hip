@@ -8,26 +8,73 @@ namespace sp {
 namespace {
 
 // ---------------------------------------------------------------- RMSNorm
+// One workgroup (256 threads) per row; the row is read once, 4 values per
+// load, and kept in registers between the sum of squares and the scaling
+// (d <= 256 * 4 * kRowChunks, d % 4 == 0).
+constexpr int kRowChunks = 8;
+
+template <typename T>
+__device__ __forceinline__ void load4(const T* p, float (&v)[4]) {
+  if constexpr (sizeof(T) == 4) {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  } else {
+    const uint2 x = *reinterpret_cast<const uint2*>(p);
+    const T* h = reinterpret_cast<const T*>(&x);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) v[e] = to_f32(h[e]);
+  }
+}
+template <typename T>
+__device__ __forceinline__ void store4(T* p, const float (&v)[4]) {
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+    T h[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = from_f32<T>(v[e]);
+    *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(h);
+  }
+}
+
 template <typename TI, typename TG, typename TO>
 __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, const TG* gain, TO* out, int d,
                                                     float eps) {
   __shared__ float red[4];
   const int r = blockIdx.x;
   const TI* xr = x + (int64_t)r * d;
+  float v[kRowChunks][4];
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    const float v = to_f32(xr[i]);
-    ss += v * v;
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int i = 4 * (threadIdx.x + 256 * c);
+    if (i < d) {
+      load4(xr + i, v[c]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ss += v[c][e] * v[c][e];
+    }
   }
   ss = block_sum_256(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
   TO* orow = out + (int64_t)r * d;
-  for (int i = threadIdx.x; i < d; i += 256) orow[i] = from_f32<TO>(to_f32(xr[i]) * inv * to_f32(gain[i]));
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int i = 4 * (threadIdx.x + 256 * c);
+    if (i < d) {
+      float gv[4];
+      load4(gain + i, gv);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[c][e] = v[c][e] * inv * gv[e];
+      store4(orow + i, v[c]);
+    }
+  }
 }
 
 // ---------------------------------------------------------------- RoPE + scatter
-// grid (k, n_q + 2 n_kv, B), hd/2 threads: thread i rotates the pair (i, i + hd/2)
-// of head h of soft row j by (N_b + j) * base^(-2i/hd), the angle in fp64.
+// One workgroup per (soft row j, sequence b): the rotation of pair (i, i + hd/2)
+// at position N_b + j by angle (N_b + j) * base^(-2i/hd) is computed once, in
+// fp64, into LDS, then applied to every query and key head of the row; the
+// value heads (no rotation, the same for every sequence) are written by b = 0.
 // SPLIT (T = bf16): each value x is stored as hi = bf16(x) and lo = bf16(x - hi).
 template <typename T, bool SPLIT>
 __device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
@@ -37,70 +84,95 @@ __device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
 }
 
 template <typename T, bool SPLIT>
-__global__ void rope_scatter(const RopeParams p) {
-  const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
+__global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
+  __shared__ float cs[64], sn[64];  // hd / 2 <= 64
+  const int j = blockIdx.x, b = blockIdx.y;
   if (p.err && *p.err) return;
   const int hd = p.hd, half = hd / 2;
-  const float* row = p.qkv + (int64_t)j * (p.n_q + 2 * p.n_kv) * hd;
-  if (h >= p.n_q + p.n_kv) {  // value head: no rotation, the same for every sequence
-    if (b != 0) return;
-    const int g = h - p.n_q - p.n_kv;
-    const int64_t base = (int64_t)g * hd * p.ks;
-    put<T, SPLIT>(p.v_soft, p.v_soft_lo, base + (int64_t)i * p.ks + j, row[h * hd + i]);
-    put<T, SPLIT>(p.v_soft, p.v_soft_lo, base + (int64_t)(i + half) * p.ks + j, row[h * hd + i + half]);
-    return;
-  }
   int n = p.seq_lens[b];
   n = n < 0 ? 0 : (n > p.max_seq_len ? p.max_seq_len : n);
-  const double theta = pow(p.rope_base, -2.0 * (double)i / (double)hd);
-  const double ang = (double)(n + j) * theta;
-  const float c = (float)cos(ang), s = (float)sin(ang);
-  const float x0 = row[h * hd + i], x1 = row[h * hd + i + half];
-  const float r0 = x0 * c - x1 * s, r1 = x1 * c + x0 * s;
-  if (h < p.n_q) {
-    const int g = h / p.group, rr = j * p.group + h % p.group;
-    const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
-    put<T, SPLIT>(p.q, p.q_lo, base + i, r0 * p.q_scale);
-    put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
-  } else {
-    constexpr int X = 16 / sizeof(T);
-    const int g = h - p.n_q;
-    const int64_t base = ((int64_t)b * p.n_kv + g) * p.ks * hd;
-    const int i1 = i + half;
-    put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + ((int64_t)(i / X) * p.ks + j) * X + i % X, r0);
-    put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + ((int64_t)(i1 / X) * p.ks + j) * X + i1 % X, r1);
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    const double theta = pow(p.rope_base, -2.0 * (double)i / (double)hd);
+    const double ang = (double)(n + j) * theta;
+    cs[i] = (float)cos(ang);
+    sn[i] = (float)sin(ang);
+  }
+  __syncthreads();
+  const float* row = p.qkv + (int64_t)j * (p.n_q + 2 * p.n_kv) * hd;
+  const int nrot = (p.n_q + p.n_kv) * half;
+  for (int e = threadIdx.x; e < nrot; e += blockDim.x) {
+    const int h = e / half, i = e % half;
+    const float c = cs[i], s = sn[i];
+    const float x0 = row[h * hd + i], x1 = row[h * hd + i + half];
+    const float r0 = x0 * c - x1 * s, r1 = x1 * c + x0 * s;
+    if (h < p.n_q) {
+      const int g = h / p.group, rr = j * p.group + h % p.group;
+      const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
+      put<T, SPLIT>(p.q, p.q_lo, base + i, r0 * p.q_scale);
+      put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
+    } else {
+      const int g = h - p.n_q;
+      const int64_t base = (((int64_t)b * p.n_kv + g) * p.ks + j) * hd;
+      put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i, r0);
+      put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i + half, r1);
+    }
+  }
+  if (b == 0) {
+    for (int e = threadIdx.x; e < p.n_kv * hd; e += blockDim.x) {
+      const int g = e / hd, i = e % hd;
+      put<T, SPLIT>(p.v_soft, p.v_soft_lo, ((int64_t)g * p.ks + j) * hd + i, row[(p.n_q + p.n_kv + g) * hd + i]);
+    }
   }
 }
 
 // ---------------------------------------------------------------- read-out
-// One workgroup per sequence: f_j = RMSNorm(y_j; gamma_final) for the read-out
-// rows (the last soft row, or all k for the mean), pooled in LDS, then
-// logits[c] = sum_i W_cls[c][i] pooled[i] (+ b[c]).
+// One workgroup per (sequence b, class c):
+//   logits[b][c] = sum_j w_j * inv_j * sum_i W_cls[c][i] gamma_i y_j[i]  (+ bias[c]),
+// with inv_j = 1 / sqrt(mean_i y_j[i]^2 + eps) over the read-out rows j (the
+// last soft row, w = 1; or all k, w = 1/k): RMSNorm, pooling and the linear
+// classifier folded into one pass and one block reduction per row.
 template <typename T>
 __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
-  extern __shared__ float pooled[];
   __shared__ float red[4];
-  const int b = blockIdx.x, d = p.d;
-  for (int i = threadIdx.x; i < d; i += 256) pooled[i] = 0.f;
+  const int b = blockIdx.x, c = blockIdx.y, d = p.d;
   const int j0 = p.pool_mean ? 0 : p.k - 1;
   const float w = p.pool_mean ? 1.0f / (float)p.k : 1.0f;
+  const T* wr = (const T*)p.w_cls + (int64_t)c * d;
+  const T* gm = (const T*)p.final_norm;
+  float wg[kRowChunks][4];  // W_cls[c][i] * gamma_i, reused for every row
+#pragma unroll
+  for (int q = 0; q < kRowChunks; ++q) {
+    const int i = 4 * (threadIdx.x + 256 * q);
+    if (i < d) {
+      float a[4], g4[4];
+      load4(wr + i, a);
+      load4(gm + i, g4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wg[q][e] = a[e] * g4[e];
+    }
+  }
+  float logit = 0.f;
   for (int j = j0; j < p.k; ++j) {
     const float* yr = p.y + ((int64_t)b * p.k + j) * d;
-    float ss = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) ss += yr[i] * yr[i];
+    float ss = 0.f, dot = 0.f;
+#pragma unroll
+    for (int q = 0; q < kRowChunks; ++q) {
+      const int i = 4 * (threadIdx.x + 256 * q);
+      if (i < d) {
+        float y4[4];
+        load4(yr + i, y4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ss += y4[e] * y4[e];
+          dot += y4[e] * wg[q][e];
+        }
+      }
+    }
     ss = block_sum_256(ss, red);
-    const float inv = 1.0f / sqrtf(ss / (float)d + p.eps);
-    for (int i = threadIdx.x; i < d; i += 256)
-      pooled[i] += yr[i] * inv * to_f32(((const T*)p.final_norm)[i]) * w;
+    dot = block_sum_256(dot, red);
+    logit += w * dot / sqrtf(ss / (float)d + p.eps);
   }
-  __syncthreads();
-  for (int c = 0; c < p.n_classes; ++c) {
-    const T* wr = (const T*)p.w_cls + (int64_t)c * d;
-    float acc = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) acc += to_f32(wr[i]) * pooled[i];
-    acc = block_sum_256(acc, red);
-    if (threadIdx.x == 0) p.logits[(int64_t)b * p.n_classes + c] = acc + (p.b_cls ? p.b_cls[c] : 0.f);
-  }
+  if (threadIdx.x == 0) p.logits[(int64_t)b * p.n_classes + c] = logit + (p.b_cls ? p.b_cls[c] : 0.f);
 }
 
 // ---------------------------------------------------------------- validation
@@ -129,6 +201,7 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
                                const void* gain, void* out, int rows, int d, float eps,
                                hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (d % 4 || d > 1024 * kRowChunks) return hipErrorInvalidValue;
   const dim3 grid(rows), block(256);
   if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
     hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, (const bf16*)gain, (f16*)out, d, eps);
@@ -142,7 +215,8 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
 }
 
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s) {
-  const dim3 grid(p.k, p.n_q + 2 * p.n_kv, batch), block(p.hd / 2);
+  if (p.hd > 128) return hipErrorInvalidValue;
+  const dim3 grid(p.k, batch), block(256);
   if (dt == kBF16)
     hipLaunchKernelGGL((rope_scatter<bf16, true>), grid, block, 0, s, p);
   else if (dt == kF32)
@@ -153,11 +227,12 @@ hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStre
 }
 
 hipError_t launch_final_classifier(DType dt, const ClsParams& p, int batch, hipStream_t s) {
-  const size_t lds = (size_t)p.d * sizeof(float);
+  if (p.d % 4 || p.d > 1024 * kRowChunks) return hipErrorInvalidValue;
+  const dim3 grid(batch, p.n_classes);
   if (dt == kBF16)
-    hipLaunchKernelGGL(final_classifier<bf16>, dim3(batch), dim3(256), lds, s, p);
+    hipLaunchKernelGGL(final_classifier<bf16>, grid, dim3(256), 0, s, p);
   else
-    hipLaunchKernelGGL(final_classifier<float>, dim3(batch), dim3(256), lds, s, p);
+    hipLaunchKernelGGL(final_classifier<float>, grid, dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
