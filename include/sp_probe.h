@@ -71,12 +71,12 @@ enum {
 
 /* Shape of the frozen head and limits of a handle. */
 typedef struct sp_probe_config {
-  int32_t hidden;        /* d: multiple of 64 (bf16) or of 4 (f32) */
+  int32_t hidden;        /* d <= 16384: multiple of 32 (bf16) or of 4 (f32) */
   int32_t n_q_heads;     /* query heads */
   int32_t n_kv_heads;    /* KV heads; n_q_heads % n_kv_heads == 0 (grouped-query attention,
                             query head h reads KV head h / (n_q_heads / n_kv_heads)) */
   int32_t head_dim;      /* 64 or 128 */
-  int32_t intermediate;  /* SwiGLU width: multiple of 64 (bf16) or of 4 (f32) */
+  int32_t intermediate;  /* SwiGLU width: multiple of 32 (bf16) or of 4 (f32) */
   int32_t k;             /* soft-prompt rows per sequence, 1..64 */
   int32_t n_classes;     /* C, 1..64 */
   int32_t dtype;         /* sp_dtype */
@@ -86,7 +86,7 @@ typedef struct sp_probe_config {
   int32_t max_batch;     /* largest batch a forward may pass */
   int32_t max_seq_len;   /* largest context length N_b a forward may pass (debug mode checks it;
                             otherwise larger values are clamped to it) */
-  int32_t split_len;     /* tokens per attention split, a power of two in [256, 16384]; 0 = automatic */
+  int32_t split_len;     /* tokens per attention split, a power of two >= 256; 0 = automatic */
   int32_t flags;         /* SP_FLAG_* */
 } sp_probe_config;
 

@@ -28,6 +28,8 @@
 //     v_mfma_f32_16x16x32_bf16 for O += P V (P never goes through LDS); the B
 //     operand is V[those 8 tokens][16nt + li], 16 contiguous LDS bytes.
 // Online softmax in log2 units with a lazy reference max (see kRescaleLog2).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -60,14 +62,18 @@ struct RowState {
 
 // One 32-token unit for one wave, in two phases.  qk_unit: kf[h][c] =
 // K[token pi_h(li)][8 (la*NC + c) ..] (the unit layout below); score i of the
-// lane (i = 4h + r) is token 8la + i for query li.  softmax_pv_unit: vf[nt] =
+// lane (i = 4h + r) is token 8la + i for query li.  The accumulators start at
+// -m (the row's reference max), so the scores come out as s - m, except in the
+// first unit of a split (FIRST), whose reference is still the -1e30 start
+// value: it takes the raw scores.  softmax_pv_unit: vf[nt] =
 // V[tokens 8la..8la+7][16nt + li]; keys at or past `limit` are masked.
-template <int HD>
+template <int HD, bool FIRST>
 __device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
                                         f32x4& s0, f32x4& s1) {
   constexpr int NC = HD / 32;
-  s0 = f32x4{0.f, 0.f, 0.f, 0.f};
-  s1 = f32x4{0.f, 0.f, 0.f, 0.f};
+  const float init = FIRST ? 0.f : -st.m;
+  s0 = f32x4{init, init, init, init};
+  s1 = s0;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     s0 = mfma16x16x32_bf16(kf[0][c], st.qh[c], s0);
@@ -77,29 +83,53 @@ __device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&k
   }
 }
 
-template <int HD>
+// p = hi + lo for two values at a time: hi = bf16(p) (round to nearest even),
+// lo = bf16(p - hi); both pairs packed as the MFMA operand expects.
+__device__ __forceinline__ void split_pair(float p0, float p1, uint32_t& hi, uint32_t& lo) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  hi = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0, p1}, bf16x2v));
+  const float h0 = __builtin_bit_cast(float, hi << 16), h1 = __builtin_bit_cast(float, hi & 0xffff0000u);
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0 - h0, p1 - h1}, bf16x2v));
+}
+
+template <int HD, bool FIRST>
 __device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x4 s1,
                                                 const bf16x8 (&vf)[HD / 16], int la, int limit) {
   constexpr int NT = HD / 16;
+  // sc = s - m, or s in the first unit
   float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
   if (limit < 32) {
 #pragma unroll
     for (int i = 0; i < 8; ++i)
       if (8 * la + i >= limit) sc[i] = -INFINITY;
   }
-  float lmax = sc[0];
-#pragma unroll
-  for (int i = 1; i < 8; ++i) lmax = fmaxf(lmax, sc[i]);
+  float lmax = fmaxf(fmaxf(sc[0], sc[1]), sc[2]);
+  lmax = fmaxf(fmaxf(lmax, sc[3]), sc[4]);
+  lmax = fmaxf(fmaxf(lmax, sc[5]), sc[6]);
+  lmax = fmaxf(lmax, sc[7]);
   // Lazy reference max: p = 2^(s - m) with m the row's reference, which only
   // moves (with the cross-lane reduction and the rescale of l and O) when some
   // score exceeds it by more than kRescaleLog2.
-  if (__any(lmax > st.m + kRescaleLog2)) {
-    lmax = fmaxf(lmax, __shfl_xor(lmax, 16));
-    lmax = fmaxf(lmax, __shfl_xor(lmax, 32));
-    const float mn = fmaxf(st.m, lmax);
-    const float alpha = fast_exp2(st.m - mn);
+  const float excess = FIRST ? lmax - st.m : lmax;
+  if (__any(excess > kRescaleLog2)) {
+    float rm = fmaxf(lmax, __shfl_xor(lmax, 16));  // the row's max (shifted or raw)
+    rm = fmaxf(rm, __shfl_xor(rm, 32));
+    float alpha;
+    if (!FIRST) {
+      const float delta = fmaxf(rm, 0.f);  // the reference moves up by delta
+      alpha = fast_exp2(-delta);
+      st.m += delta;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sc[i] -= delta;
+    } else {
+      const float mn = fmaxf(st.m, rm);
+      alpha = fast_exp2(st.m - mn);
+      st.m = mn;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sc[i] -= mn;
+    }
     st.l *= alpha;
-    st.m = mn;
     // O rows held by this lane are queries 4la + r; their factors live in lanes 4la + r.
     float ar[4];
 #pragma unroll
@@ -108,17 +138,23 @@ __device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) st.o[nt][r] *= ar[r];
+  } else if (FIRST) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) sc[i] -= st.m;
   }
-  bf16x8 ph, pl;
+  float pv[8];
   float ps = 0.f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const float pv = fast_exp2(sc[i] - st.m);
-    ps += pv;
-    ph[i] = (bf16)pv;
-    pl[i] = (bf16)(pv - (float)ph[i]);
+    pv[i] = fast_exp2(sc[i]);
+    ps += pv[i];
   }
   st.l += ps;
+  uint32_t hw[4], lw[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) split_pair(pv[2 * q], pv[2 * q + 1], hw[q], lw[q]);
+  const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
+  const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     st.o[nt] = mfma16x16x32_bf16(ph, vf[nt], st.o[nt]);
@@ -160,9 +196,16 @@ struct UnitLayout {
   }
 };
 
-// Longest split of the bf16 path: its physical block ids are staged in LDS.
-constexpr int kMaxSplitBf16 = 16384;
-constexpr int kMaxSplitBlocks = kMaxSplitBf16 / 16 + 1;  // block size >= 16, t0 maybe mid-block
+// The split's physical block ids live in LDS in a rolling table of two windows
+// of kIdWin logical blocks (window w in slot w & 1).
+constexpr int kIdWin = 512;
+
+// Direct global -> LDS load of 4 bytes per lane (lane l's at wave_dst + 4 l);
+// waited for like ld16_to_lds.
+__device__ __forceinline__ void ld4_to_lds(const void* base, uint32_t lane_off, int* wave_dst) {
+  const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) int*)wave_dst;
+  asm volatile("global_load_lds_dword %0, %1" : : "v"(lane_off), "s"(base), "{m0}"(lds) : "memory");
+}
 
 // Zero the V values of tokens at or past `limit` in a staged tail unit (the
 // bytes there may be anything, NaN included, and P V would carry 0 * NaN).
@@ -184,7 +227,7 @@ __device__ __forceinline__ void zero_tail(u32x4* sb, int limit, int tid) {
 }
 
 // A wave's fragments of a staged unit, then the unit's softmax and products.
-template <int HD>
+template <int HD, bool FIRST>
 __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, int limit, int li,
                                              int la) {
   constexpr int NC = HD / 32, NT = HD / 16;
@@ -196,7 +239,7 @@ __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, 
 #pragma unroll
       for (int c = 0; c < NC; ++c)
         kf[h][c] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::k_piece(h, la * NC + c, li)]);
-    qk_unit<HD>(st, kf, s0, s1);
+    qk_unit<HD, FIRST>(st, kf, s0, s1);
   }
   // V fragments are read only once the QK products are issued, into the
   // registers the K fragments held.
@@ -205,7 +248,7 @@ __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, 
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
     vf[nt] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::v_piece(nt, li, la)]);
-  softmax_pv_unit<HD>(st, s0, s1, vf, la, limit);
+  softmax_pv_unit<HD, FIRST>(st, s0, s1, vf, la, limit);
 }
 
 // W waves per workgroup, one per 16-row query tile.  Three LDS stages: unit u
@@ -217,7 +260,7 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   constexpr int PPL = (NI + W - 1) / W;  // wave-instructions per wave per unit
   static_assert(W <= 2 * NI, "a wave must have at least one distinct instruction slot");
   __shared__ u32x4 stage[3][UnitLayout<HD>::PIECES];
-  __shared__ int blk_ids[kMaxSplitBlocks];   // physical block of each logical block of the split
+  __shared__ int blk_ids[2][kIdWin];  // physical blocks of the split (rolling windows)
 
   const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, la = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -252,10 +295,26 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   if (nunits > 0) {
     const bf16* kbase = (const bf16*)p.k_base + (int64_t)g * p.k_sh;
     const bf16* vbase = (const bf16*)p.v_base + (int64_t)g * p.v_sh;
+    // Physical block of logical block lb0 + rel: windows 0 and 1 are read now;
+    // window w + 1 is loaded (direct loads into LDS, one wave-instruction per
+    // 64 ids) when issuing enters window w, kIdWin blocks before it is needed.
+    // A unit's two halves always fall in one window (rel of its first half is
+    // even: t0 is a multiple of 32 tokens, blocks hold >= 16).
     const int lb0 = t0 >> p.bs_log2;
     const int nlb = ((t1 - 1) >> p.bs_log2) - lb0 + 1;
-    for (int i = tid; i < min(nlb, kMaxSplitBlocks); i += 64 * W)
-      blk_ids[i] = p.block_table ? p.block_table[(int64_t)b * p.mbps + lb0 + i] : b * p.mbps + lb0 + i;
+    const int* bt_row = p.block_table ? p.block_table + (int64_t)b * p.mbps + lb0 : nullptr;
+    if (bt_row)
+      for (int i = tid; i < min(nlb, 2 * kIdWin); i += 64 * W) blk_ids[i / kIdWin][i % kIdWin] = bt_row[i];
+    auto phys = [&](int rel) __attribute__((always_inline)) -> int64_t {
+      return bt_row ? (int64_t)__builtin_amdgcn_readfirstlane(blk_ids[(rel / kIdWin) & 1][rel % kIdWin])
+                    : (int64_t)b * p.mbps + lb0 + rel;
+    };
+    auto load_window = [&](int w) __attribute__((always_inline)) {
+      for (int j = wave; j < kIdWin / 64; j += W) {
+        const int rel = min(w * kIdWin + j * 64 + lane, nlb - 1);  // past the end: re-read the last id
+        ld4_to_lds(bt_row, (uint32_t)rel * 4u, &blk_ids[w & 1][j * 64]);
+      }
+    };
     // Nothing the compiler tracks stays in flight past this point (the Q loads
     // included), so it never waits on the vector-memory counter inside the loop,
     // where the counter also holds the direct-to-LDS loads.
@@ -288,8 +347,7 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     auto issue = [&](int u, int buf) __attribute__((always_inline)) {
       const int ta = t0 + 32 * u;
       const int tb = ta + 16 < t1 ? ta + 16 : ta;
-      const int64_t ba = __builtin_amdgcn_readfirstlane(blk_ids[(ta >> p.bs_log2) - lb0]);
-      const int64_t bb = __builtin_amdgcn_readfirstlane(blk_ids[(tb >> p.bs_log2) - lb0]);
+      const int64_t ba = phys((ta >> p.bs_log2) - lb0), bb = phys((tb >> p.bs_log2) - lb0);
       const int sa = ta & (bs - 1), sbb = tb & (bs - 1);
       const bf16* g0 = kbase + ba * p.k_sb + sa * 8;
       const bf16* g1 = kbase + bb * p.k_sb + sbb * 8;
@@ -306,7 +364,9 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     issue(0, 0);
     if (last >= 1) issue(1, 1);
     int buf = 0;
-    for (int u = 0; u < nunits; ++u) {
+    // One unit: wait for its loads, publish them, issue unit u + 2, compute.
+    // The first unit is peeled (raw scores; see qk_unit).
+    auto step = [&](int u, auto first) __attribute__((always_inline)) {
       // this wave's loads of unit u are done once at most those of unit u + 1 remain
       if (u < last)
         wait_vmcnt<PPL>();
@@ -319,10 +379,20 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
         zero_tail<HD, W>(stage[buf], limit, tid);
         lds_barrier();
       }
-      if (u + 2 <= last) issue(u + 2, buf == 0 ? 2 : buf - 1);
-      compute_unit<HD>(st, stage[buf], limit, li, la);
+      if (u + 2 <= last) {
+        issue(u + 2, buf == 0 ? 2 : buf - 1);
+        // entering window w >= 1 of the block ids: load window w + 1 (it
+        // replaces window w - 1, which no later unit reads).  Loads issued
+        // after the unit's only make the next vmcnt waits stricter.
+        const int w = (((t0 + 32 * (u + 2)) >> p.bs_log2) - lb0) / kIdWin;
+        const int wprev = (((t0 + 32 * (u + 1)) >> p.bs_log2) - lb0) / kIdWin;
+        if (bt_row && w != wprev && (w + 1) * kIdWin < nlb) load_window(w + 1);
+      }
+      compute_unit<HD, decltype(first)::value>(st, stage[buf], limit, li, la);
       buf = buf == 2 ? 0 : buf + 1;
-    }
+    };
+    step(0, std::true_type{});
+    for (int u = 1; u < nunits; ++u) step(u, std::false_type{});
   }
 
   const int64_t prow = (((int64_t)b * p.n_kv + g) * p.max_splits + s) * p.r_alloc + row0;
@@ -546,7 +616,7 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
 }  // namespace
 
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
-  if (p.split_len > kMaxSplitBf16 || p.bs_log2 < 4) return hipErrorInvalidValue;
+  if (p.bs_log2 < 4 || p.split_len % 32) return hipErrorInvalidValue;
   const dim3 grid(p.max_splits, p.n_kv * p.n_qgroups, batch);
 #define SP_ATTN_CASE(HD_, W_)                                                          \
   if (hd == HD_ && waves == W_) {                                                      \

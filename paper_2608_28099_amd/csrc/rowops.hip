@@ -10,8 +10,8 @@ namespace {
 // ---------------------------------------------------------------- RMSNorm
 // One workgroup (256 threads) per row; the row is read once, 4 values per
 // load, and kept in registers between the sum of squares and the scaling
-// (d <= 256 * 4 * kRowChunks, d % 4 == 0).
-constexpr int kRowChunks = 8;
+// (d <= 256 * 4 * kRowChunks = 16384, d % 4 == 0).
+constexpr int kRowChunks = 16;
 
 template <typename T>
 __device__ __forceinline__ void load4(const T* p, float (&v)[4]) {

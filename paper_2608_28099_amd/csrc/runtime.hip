@@ -10,6 +10,8 @@
 #include "../../include/sp_probe.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 #define SP_API extern "C" __attribute__((visibility("default")))
 
 namespace {
@@ -40,12 +42,11 @@ int check_config(const sp_probe_config* c) {
     return SP_ERR_INVALID_ARG;
   if (c->n_q_heads % c->n_kv_heads) return SP_ERR_INVALID_ARG;
   if (!(c->rms_eps >= 0.0f) || !(c->rope_base > 0.0)) return SP_ERR_INVALID_ARG;
-  if (c->split_len != 0 && (c->split_len < 256 || c->split_len > 16384 || !is_pow2(c->split_len)))
-    return SP_ERR_INVALID_ARG;
+  if (c->split_len != 0 && (c->split_len < 256 || !is_pow2(c->split_len))) return SP_ERR_INVALID_ARG;
   if (c->flags & ~(SP_FLAG_DEBUG | SP_FLAG_PROFILE)) return SP_ERR_INVALID_ARG;
   if (c->head_dim != 64 && c->head_dim != 128) return SP_ERR_UNSUPPORTED;
   if (c->k > 64 || c->n_classes > 64) return SP_ERR_UNSUPPORTED;
-  const int mult = c->dtype == SP_BF16 ? 64 : 4;
+  const int mult = c->dtype == SP_BF16 ? 32 : 4;
   if (c->hidden % mult || c->intermediate % mult) return SP_ERR_UNSUPPORTED;
   if (c->dtype == SP_F32 && c->k * (c->n_q_heads / c->n_kv_heads) > 64) return SP_ERR_UNSUPPORTED;
   if (c->hidden > 16384) return SP_ERR_UNSUPPORTED;
@@ -81,8 +82,22 @@ Plan make_plan(const sp_probe_config& c) {
   p.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   if (c.split_len) {
     p.split_len = c.split_len;
+  } else if (c.dtype == SP_BF16) {
+    // Splits sized so that the attention grid at the full batch and length is
+    // about one round of resident workgroups (256 compute units x 3 workgroups
+    // of <= 4 waves, x 2 above): every round of workgroups costs a start-up
+    // and a drain.  At most max_seq_len / 2 (two splits for the longest
+    // sequence, so batches of mixed lengths still balance), at least 1024,
+    // a multiple of 256.
+    const int64_t slots = 256 * (p.waves <= 4 ? 3 : 2);
+    const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * p.n_qgroups;
+    const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
+    const int64_t half = ((int64_t)c.max_seq_len / 2 + 255) / 256 * 256;
+    int64_t sl = (want + 255) / 256 * 256;
+    sl = std::min(sl, half);
+    p.split_len = (int)std::max<int64_t>(sl, 1024);
   } else {
-    // at most 8 splits per sequence, between 1024 and 16384 tokens each
+    // fp32 path: at most 8 splits per sequence, between 1024 and 16384 tokens each
     int sl = 1024;
     while (sl < 16384 && (int64_t)sl * 8 < c.max_seq_len) sl *= 2;
     p.split_len = sl;

@@ -91,7 +91,7 @@ def test_workspace_sizing(name):
 def test_invalid_configs_are_rejected_without_a_device():
     w = configs.SMALL_BF16
     bad = [dict(head_dim=96), dict(n_kv_heads=3), dict(k=0), dict(k=65), dict(n_classes=0),
-           dict(hidden=500), dict(intermediate=100), dict(split_len=300), dict(split_len=128), dict(split_len=32768),
+           dict(hidden=500), dict(intermediate=100), dict(split_len=300), dict(split_len=128),
            dict(max_batch=0), dict(dtype=7), dict(flags=8)]
     for kw in bad:
         cfg = binding.make_config(w)

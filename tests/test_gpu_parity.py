@@ -128,6 +128,29 @@ def test_head_dims_and_splits(hd, dev):
         probe.close()
 
 
+def test_projection_tile_shapes(dev):
+    """Shapes whose projections select the fallback tiles of the bf16 GEMM:
+    64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, and the
+    32-deep K step (width 4128 is not a multiple of 64) with head_dim 64."""
+    cases = [
+        configs.Workload(name="tiles_a", dtype="bf16", batch=16, k=16, hidden=4096, n_q_heads=8,
+                         n_kv_heads=2, head_dim=128, intermediate=1024, n_classes=3,
+                         seq_len=("uniform", 1, 300), seed=50),
+        configs.Workload(name="tiles_b", dtype="bf16", batch=4, k=8, hidden=4128, n_q_heads=4,
+                         n_kv_heads=2, head_dim=64, intermediate=512, n_classes=2,
+                         seq_len=("list", (257, 64, 0, 33)), seed=51),
+    ]
+    for w in cases:
+        announce(f"[tiles] {w.name}")
+        kv, params, kv_d, p_d = small_case(w, dev)
+        probe = binding.Probe(w)
+        got = probe.forward(kv_d, p_d).cpu().numpy()
+        ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+        err = H.check_logits(got, ref, w.dtype, w.name)
+        announce(f"[tiles] {w.name}: max err {err:.3e}")
+        probe.close()
+
+
 # ---------------------------------------------------------------- invariances (bitwise)
 
 def test_invariances_are_bitwise(dev):
