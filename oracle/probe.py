@@ -32,6 +32,10 @@ Readings of points the paper leaves open (one pass instead of the recursive
 chaining, soft prompt fed straight into the layer, the layer's internals,
 causal mask among the soft rows, post-RoPE cached keys, contiguous GQA
 grouping) are listed with the design notes of the repository.
+
+The recursive form the paper evaluates (SP-k: the MTP input fusion of
+Sec. 3.1, chained over k steps as in Sec. 3.2) is ``probe_sequence_recursive``
+at the end of this module.
 """
 from __future__ import annotations
 
@@ -164,5 +168,106 @@ def probe_batch(kv_list, soft_prompt, weights: dict, shape: HeadShape, taps: boo
 
     Every sequence is classified on its own (Sec. 3.3): the batch is a loop."""
     outs = [probe_sequence(kc, vc, soft_prompt, weights, shape) for kc, vc in kv_list]
+    logits = np.stack([o["logits"] for o in outs]) if outs else np.zeros((0, f64(weights["w_cls"]).shape[0]))
+    return (logits, outs) if taps else logits
+
+
+# ---------------------------------------------------------------- recursive SP-k
+#
+# Sec. 3.1 (MTP architecture) and Sec. 3.2 (recursive soft prompts): the head's
+# input at a position is the projection W_fc [RMSNorm(h; gamma_h);
+# RMSNorm(e; gamma_e)] of a hidden state h and an embedding e; SP-k replaces the
+# embedding of step i with the learned vector e_i, takes the base model's last
+# hidden state as h for the first step and the head's own output hidden state
+# of step i-1 for every later step, and classifies the output of step k.
+#
+# Readings (the paper leaves them open):
+#   * w_fc is stored [d][2d]; its columns 0..d-1 multiply the normed hidden
+#     state and columns d..2d-1 the normed soft-prompt vector (the order in
+#     which Sec. 3.1 lists the two inputs);
+#   * the "output hidden state" a step hands on (and the one the classifier
+#     reads) is the final-normed f_t;
+#   * step t (0-based) sits at position N + t and attends to the N cached keys
+#     plus the soft keys of steps 0..t (its own included);
+#   * the read-out options are those of the one-pass form: f of the last step,
+#     or the mean of f over the k steps.
+
+def recursive_step(x_t, t, n, k_cache, v_cache, soft_k, soft_v, W, shape):
+    """One application of the decoder layer to the fused input x_t [d] at
+    position n + t.  soft_k / soft_v (lists of [n_kv, hd]) hold the rotated soft
+    keys and the values of steps 0..t-1 and receive this step's.  Returns the
+    step's taps (x, q_rot, probabilities, o, a, s, y, f)."""
+    hq, hkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
+    group = hq // hkv
+    u = rms_norm(x_t, W["in_norm"], shape.rms_eps)
+    q = (W["w_q"] @ u).reshape(1, hq, hd)
+    kap = (W["w_k"] @ u).reshape(1, hkv, hd)
+    v = (W["w_v"] @ u).reshape(hkv, hd)
+    pos = np.array([n + t])
+    q_rot = rope(q, pos, shape.rope_base)[0]
+    soft_k.append(rope(kap, pos, shape.rope_base)[0])
+    soft_v.append(v)
+    keys_soft = np.stack(soft_k)                    # [t+1, n_kv, hd]
+    vals_soft = np.stack(soft_v)
+    kc, vc = f64(k_cache), f64(v_cache)
+    o = np.empty((hq, hd))
+    probs = []
+    for h in range(hq):
+        g = h // group
+        keys = np.concatenate([kc[g], keys_soft[:, g, :]])     # [n + t + 1, hd]
+        vals = np.concatenate([vc[g], vals_soft[:, g, :]])
+        p = softmax_rows((keys @ q_rot[h] / np.sqrt(hd))[None, :])[0]
+        o[h] = p @ vals
+        probs.append(p)
+    a = x_t + W["w_o"] @ o.reshape(hq * hd)
+    w_in = rms_norm(a, W["post_norm"], shape.rms_eps)
+    s = silu(W["w_gate"] @ w_in) * (W["w_up"] @ w_in)
+    y = a + W["w_down"] @ s
+    f = rms_norm(y, W["final_norm"], shape.rms_eps)
+    return {"x": x_t, "q_rot": q_rot, "probs": probs, "o": o.reshape(hq * hd), "a": a, "s": s,
+            "y": y, "f": f}
+
+
+def probe_sequence_recursive(k_cache, v_cache, soft_prompt, h_last, weights: dict,
+                             shape: HeadShape) -> dict:
+    """Recursive SP-k logits and per-step values for one sequence.
+
+    k_cache, v_cache: [n_kv, N, hd]; soft_prompt: [k, d] (e_1..e_k); h_last: [d],
+    the base model's last hidden state; weights: the one-pass keys plus
+    fc_norm_h [d], fc_norm_e [d] and w_fc [d][2d].  Returned arrays stack the
+    steps: x, a, y, f are [k, d], o is [k, n_q*hd]."""
+    W = {key: (None if val is None else f64(val)) for key, val in weights.items()}
+    e = f64(soft_prompt)
+    k, d = e.shape
+    n = int(np.shape(k_cache)[1])
+    h = f64(h_last)
+    soft_k, soft_v, steps = [], [], []
+    for t in range(k):
+        z = np.concatenate([rms_norm(h, W["fc_norm_h"], shape.rms_eps),
+                            rms_norm(e[t], W["fc_norm_e"], shape.rms_eps)])
+        x_t = W["w_fc"] @ z
+        st = recursive_step(x_t, t, n, k_cache, v_cache, soft_k, soft_v, W, shape)
+        steps.append(st)
+        h = st["f"]
+    f = np.stack([st["f"] for st in steps])
+    if shape.pool == "last":
+        pooled = f[k - 1]
+    elif shape.pool == "mean":
+        pooled = np.mean(f, axis=0)
+    else:
+        raise ValueError(shape.pool)
+    logits = W["w_cls"] @ pooled
+    if W.get("b_cls") is not None:
+        logits = logits + W["b_cls"]
+    out = {name: np.stack([st[name] for st in steps]) for name in ("x", "o", "a", "y", "f")}
+    out.update({"probs": [st["probs"] for st in steps], "pooled": pooled, "logits": logits})
+    return out
+
+
+def probe_batch_recursive(kv_list, soft_prompt, h_last, weights: dict, shape: HeadShape,
+                          taps: bool = False):
+    """Recursive SP-k logits [B, C]; h_last [B, d] holds each sequence's last base hidden state."""
+    outs = [probe_sequence_recursive(kc, vc, soft_prompt, h_last[b], weights, shape)
+            for b, (kc, vc) in enumerate(kv_list)]
     logits = np.stack([o["logits"] for o in outs]) if outs else np.zeros((0, f64(weights["w_cls"]).shape[0]))
     return (logits, outs) if taps else logits

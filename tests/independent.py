@@ -88,3 +88,29 @@ def textbook_decode(q, keys, values):
         for i in range(hd):
             out[i] += wt / tot * float(vt[i])
     return np.array(out)
+
+
+def draft_without_cache(x_ctx, e, h_last, weights, n_q, n_kv, hd, eps, base):
+    """Recursive SP-k computed the way a head without a KV cache would draft:
+    every step re-runs ``full_layer`` over the whole sequence [context rows;
+    fused rows of steps 0..t] and keeps the last row.  The fused row of step t
+    is w_fc applied to the two normed inputs stacked as (hidden, soft vector),
+    the hidden being the base model's last state for t = 0 and the previous
+    step's final-normed output after that.
+
+    Returns dict: x [k, d] fused rows, f [k, d] final-normed outputs of the
+    steps, and the full_layer result of the last step (rows N.. are the steps)."""
+    W = {k: (None if v is None else np.asarray(v, np.float64)) for k, v in weights.items()}
+    x_ctx = np.asarray(x_ctx, np.float64).reshape(-1, np.shape(e)[1])
+    e = np.asarray(e, np.float64)
+    hid = np.asarray(h_last, np.float64)
+    rows, outs, last = [], [], None
+    for t in range(e.shape[0]):
+        stacked = np.concatenate([_rms(hid[None], W["fc_norm_h"], eps)[0],
+                                  _rms(e[t][None], W["fc_norm_e"], eps)[0]])
+        row = np.einsum("ij,j->i", W["w_fc"], stacked)
+        rows.append(row)
+        last = full_layer(np.concatenate([x_ctx, np.stack(rows)]), W, n_q, n_kv, hd, eps, base)
+        hid = last["f"][-1]
+        outs.append(hid)
+    return {"x": np.stack(rows), "f": np.stack(outs), "last": last}
