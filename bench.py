@@ -3,6 +3,9 @@
 One step = one sp_probe_forward over the whole batch of the workload (soft-row
 prep, split attention over the paged KV cache, merge, o-projection, norm,
 SwiGLU MLP, final norm and classifier), inputs already resident in HBM.
+--mode recursive: one step = one sp_probe_forward_recursive (recursive SP-k
+with the MTP input fusion: k single-row passes of the head, each reading the
+whole cache once) on the recursive workload.
 
 Prints one JSON line:
   value      classifications/s = batch / (wall time per step), timed over K steps
@@ -28,9 +31,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = "classifications/sec at 1 MI355X; attention KV-read GB/s as % of HBM peak"
 HBM_PEAK_GBPS = 8000.0
-DEFAULT_WORKLOAD = "long_9b_bf16"
+DEFAULT_WORKLOAD = {"one-pass": "long_9b_bf16", "recursive": "long_9b_bf16_sp5"}
 ATTN_SRC = os.path.join(ROOT, "paper_2608_28099_amd", "csrc", "attention.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_long_9b_bf16_traffic.json")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def parse():
@@ -38,7 +41,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--mode", choices=("one-pass", "recursive"), default="one-pass")
+    ap.add_argument("--workload", default=None)
     ap.add_argument("--split-len", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -52,11 +56,11 @@ def attention_source_hash() -> str:
     return hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()[:16]
 
 
-def traffic_per_launch():
-    """HBM bytes per attention launch from committed counter runs, if they were
-    taken on the current attention source; else None."""
+def traffic_per_launch(workload: str):
+    """HBM bytes per attention launch from committed counter runs on this
+    workload, if they were taken on the current attention source; else None."""
     try:
-        rec = json.load(open(TRAFFIC_FILE))
+        rec = json.load(open(os.path.join(PROFILES, f"attention_{workload}_traffic.json")))
     except (OSError, ValueError):
         return None
     if rec.get("attention_src_sha256_16") != attention_source_hash():
@@ -64,13 +68,19 @@ def traffic_per_launch():
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, kv, params, seconds: float):
-    """The oracle, as written, timed on the host over whole sequences of the workload."""
+def cpu_baseline(w, kv, params, seconds: float, fusion=None):
+    """The oracle, as written, timed on the host over whole sequences of the
+    workload (the recursive oracle when fusion inputs are given)."""
     import numpy as np
     import threadpoolctl
 
     from oracle import probe as oracle
     W = {k: (None if v is None else v.double().cpu().numpy()) for k, v in params.items() if k != "soft_prompt"}
+    if fusion is not None:
+        W.update({"fc_norm_h": fusion["fc_norm_hidden"].double().cpu().numpy(),
+                  "fc_norm_e": fusion["fc_norm_embed"].double().cpu().numpy(),
+                  "w_fc": fusion["w_fc"].double().cpu().numpy()})
+        h_last = fusion["hidden_last"].double().cpu().numpy()
     soft = params["soft_prompt"].double().cpu().numpy()
     shape = oracle.HeadShape(w.n_q_heads, w.n_kv_heads, w.head_dim, w.rms_eps, w.rope_base, w.pool)
     threads = max((i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()), default=1)
@@ -79,7 +89,10 @@ def cpu_baseline(w, kv, params, seconds: float):
         k, v = kv.logical_kv(b)
         k, v = k.double().cpu().numpy(), v.double().cpu().numpy()
         t = time.perf_counter()
-        oracle.probe_sequence(k, v, soft, W, shape)
+        if fusion is None:
+            oracle.probe_sequence(k, v, soft, W, shape)
+        else:
+            oracle.probe_sequence_recursive(k, v, soft, h_last[b], W, shape)
         spent += time.perf_counter() - t
         done += 1
         toks += k.shape[1]
@@ -112,17 +125,26 @@ def main():
         print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 3}))
         return
 
-    w = configs.WORKLOADS.get(args.workload) or configs.STRESS[args.workload]
+    recursive = args.mode == "recursive"
+    name = args.workload or DEFAULT_WORKLOAD[args.mode]
+    w = configs.WORKLOADS.get(name) or configs.STRESS.get(name) or configs.RECURSIVE[name]
     print(f"[bench] {w.name}: generating inputs on the GPU", file=sys.stderr, flush=True)
     lens = inputs.seq_lens(w)
     kv = inputs.kv_cache(w, lens, dev)
     params = inputs.params(w, dev)
+    fusion = inputs.fusion_params(w, dev) if recursive else None
     logits = torch.empty((w.batch, w.n_classes), dtype=torch.float32, device=dev)
     probe = binding.Probe(w, split_len=args.split_len, flags=binding.SP_FLAG_PROFILE)
     torch.cuda.synchronize()
 
+    def step():
+        if recursive:
+            probe.forward_recursive(kv, params, fusion, logits)
+        else:
+            probe.forward(kv, params, logits)
+
     for _ in range(args.warmup):
-        probe.forward(kv, params, logits)
+        step()
     torch.cuda.synchronize()
     probe.profile_read()  # discard warm-up events
 
@@ -130,26 +152,28 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        probe.forward(kv, params, logits)
+        step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    # the event pool keeps the last forwards that fit (all of them at these step counts)
     stages, n_fwd = probe.profile_read()
-    assert n_fwd == args.steps
+    assert 0 < n_fwd <= args.steps
     ms_per_step = 1000.0 * elapsed / args.steps
     assert bool(torch.isfinite(logits).all()), "non-finite logits"
 
     esz = 2 if w.dtype == "bf16" else 4
     kv_bytes = int(lens.astype("int64").sum()) * w.n_kv_heads * w.head_dim * 2 * esz
-    attn_ms = stages["attention"] / n_fwd
+    launches = w.k if recursive else 1   # attention launches per step
+    attn_ms = stages["attention"] / (n_fwd * launches)
     achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = traffic_per_launch()
+    traffic = traffic_per_launch(w.name)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": "attn_split_bf16" if w.dtype == "bf16" else "attn_split_f32",
                 "algorithmic_bytes_per_launch": kv_bytes, "mean_launch_ms": round(attn_ms, 4)}
-    plan = probe.plan(w.batch)
+    plan = probe.plan_recursive(w.batch) if recursive else probe.plan(w.batch)
     out = {
-        "metric": METRIC, "value": round(w.batch / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
+        "metric": METRIC if not recursive else "recursive SP-k classifications/sec at 1 MI355X", "value": round(w.batch / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic (seeded; random-init head weights; paged KV ~N(0,1))",
@@ -157,7 +181,8 @@ def main():
                    "hidden": w.hidden, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "intermediate": w.intermediate, "n_classes": w.n_classes,
                    "kv_layout": w.layout, "block_size": kv.block_size, "kv_bytes": kv_bytes,
-                   "split_len": plan["split_len"], "parallelism": "single GPU"},
+                   "split_len": plan["split_len"], "parallelism": "single GPU",
+                   "mode": args.mode, "attention_launches_per_step": launches},
         "roofline": roofline,
         "attention_gbps": round(achieved, 1),
         "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},
@@ -165,7 +190,7 @@ def main():
     probe.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds, fusion)
     print(json.dumps(out), flush=True)
 
 

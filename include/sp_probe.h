@@ -12,6 +12,8 @@
  *     final RMSNorm -> read-out row(s) -> linear classifier -> logits[b, 0..C-1].
  * The new rows' keys and values live in a library-owned scratch area and are
  * never written into the caller's cache (Sec. 3.3, last paragraph).
+ * sp_probe_forward_recursive runs the recursive form (SP-k with the MTP input
+ * fusion, Sec. 3.1-3.2): k single-row steps, each fed the previous step's output.
  *
  * Conventions
  *  - Every pointer named "device" is a device address on the current HIP
@@ -156,21 +158,55 @@ int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv_cache, const int32_t* 
                      const int32_t* block_table, const void* soft_prompt,
                      const sp_probe_weights* weights, float* logits, void* stream);
 
+/* The MTP input fusion of the head (Sec. 3.1): the layer's input at a position
+ * is W_fc [RMSNorm(h; gamma_h); RMSNorm(e; gamma_e)] for a hidden state h and an
+ * embedding e.  Device pointers in the config's dtype, 16-byte aligned:
+ *   fc_norm_hidden[d] = gamma_h, fc_norm_embed[d] = gamma_e,
+ *   w_fc[d][2d] row-major: columns 0..d-1 multiply the normed hidden state,
+ *   columns d..2d-1 the normed embedding (a checkpoint that stores the other
+ *   order is passed with its two column halves swapped). */
+typedef struct sp_probe_fusion {
+  const void* fc_norm_hidden;
+  const void* fc_norm_embed;
+  const void* w_fc;
+} sp_probe_fusion;
+
+/* Recursive SP-k, the form the paper evaluates (Sec. 3.2, with the fusion of
+ * Sec. 3.1): k steps of the head, one row per sequence each.  Step t = 0..k-1
+ * takes the fused row x_t = W_fc [RMSNorm(h_t; gamma_h); RMSNorm(e_t; gamma_e)]
+ * with e_t = soft_prompt row t, h_0 = hidden_last[b] (the base model's last
+ * hidden state) and h_t = f_{t-1} (the final-normed output of the step before);
+ * it sits at position N_b + t and attends to the N_b cached keys plus the soft
+ * keys of steps 0..t.  The read-out is the config's pool over the steps' f_t
+ * (SP_POOL_LAST: f_{k-1}, the output of the k-th step).  The cache is read once
+ * per step.
+ *   hidden_last  device [B][d] in the config's dtype
+ *   fusion       host struct of device pointers
+ * Every other argument, the checks and the error behaviour are those of
+ * sp_probe_forward; the same handle serves both forwards. */
+int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv_cache, const int32_t* seq_lens,
+                               const int32_t* block_table, const void* soft_prompt,
+                               const void* hidden_last, const sp_probe_fusion* fusion,
+                               const sp_probe_weights* weights, float* logits, void* stream);
+
 /* Free the workspace and the handle (waits for the device). NULL is accepted. */
 int sp_probe_destroy(sp_probe_t* h);
 
 /* Human-readable name of a status code (static string). */
 const char* sp_probe_status_string(int status);
 
-/* Intermediate values of the last forward, for tests.  tap selects:
+/* Intermediate values of the last forward, for tests.  Row b*k + j is soft row
+ * j (one-pass) or step j (recursive) of sequence b.  tap selects:
  *   SP_TAP_QKV   fp32 [k][(n_q + 2 n_kv) hd]   projections of the normed soft rows
- *   SP_TAP_ATTN  [B k][n_q hd]                 attention output, row b*k + j (fp16 for
- *                                              SP_BF16, fp32 for SP_F32)
+ *                                              (one-pass forward only)
+ *   SP_TAP_ATTN  [B k][n_q hd]                 attention output (fp16 for SP_BF16,
+ *                                              fp32 for SP_F32)
  *   SP_TAP_A     fp32 [B k][d]                 residual after the o-projection
  *   SP_TAP_Y     fp32 [B k][d]                 residual after the MLP
+ *   SP_TAP_X     fp32 [B k][d]                 fused input rows x_t (recursive forward only)
  * sp_probe_tap_bytes returns the size for a batch; sp_probe_copy_tap enqueues a
  * device-to-device copy of it into dst (device, dst_bytes >= that size). */
-enum { SP_TAP_QKV = 0, SP_TAP_ATTN = 1, SP_TAP_A = 2, SP_TAP_Y = 3 };
+enum { SP_TAP_QKV = 0, SP_TAP_ATTN = 1, SP_TAP_A = 2, SP_TAP_Y = 3, SP_TAP_X = 4 };
 size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch);
 int sp_probe_copy_tap(sp_probe_t* h, int tap, int32_t batch, void* dst, size_t dst_bytes, void* stream);
 
@@ -179,11 +215,14 @@ int sp_probe_copy_tap(sp_probe_t* h, int tap, int32_t batch, void* dst, size_t d
 int sp_probe_check_device_error(sp_probe_t* h, void* stream);
 
 /* Profiling mode: per-stage device time summed over the forwards since the last
- * read (waits for them).  Stages, in order: 0 soft-row prep (norm, QKV, RoPE),
- * 1 split attention, 2 split merge, 3 o-projection, 4 post-attention norm,
- * 5 gate/up + SwiGLU, 6 down projection, 7 final norm + classifier.
- * stage_ms[n_stages] receives milliseconds, *n_forwards the number of forwards
- * counted (at most the last 256). */
+ * read (waits for them).  Stages, in order: 0 soft-row prep (norm, QKV, RoPE;
+ * recursive: with the fusion), 1 split attention, 2 split merge, 3 o-projection,
+ * 4 post-attention norm, 5 gate/up + SwiGLU, 6 down projection, 7 final norm +
+ * classifier (recursive: the final norm of every step); a recursive forward adds
+ * its k steps into the same stages.  stage_ms[n_stages] receives milliseconds,
+ * *n_forwards the number of forwards counted: the last ones whose events fit a
+ * pool of 256 * (SP_N_STAGES + 1) (256 one-pass forwards; 2304 / (8k + 1)
+ * recursive ones). */
 #define SP_N_STAGES 8
 int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stages, int32_t* n_forwards);
 
@@ -191,6 +230,9 @@ int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stages, int3
  * the split-attention kernel for a batch (for measurement and tests). */
 int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len, int32_t* max_splits,
                   int32_t* rows_per_kv_head, int32_t* query_groups);
+/* The same for the attention of a recursive step (G query rows per KV head). */
+int sp_probe_plan_recursive(const sp_probe_t* h, int32_t batch, int32_t* split_len,
+                            int32_t* max_splits, int32_t* rows_per_kv_head, int32_t* query_groups);
 
 #ifdef __cplusplus
 }

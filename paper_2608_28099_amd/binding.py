@@ -20,14 +20,15 @@ STATUS = {0: "SP_OK", -1: "SP_ERR_INVALID_ARG", -2: "SP_ERR_UNSUPPORTED", -3: "S
 SP_F32, SP_BF16 = 0, 1
 SP_POOL_LAST, SP_POOL_MEAN = 0, 1
 SP_FLAG_DEBUG, SP_FLAG_PROFILE = 1, 2
-SP_TAP_QKV, SP_TAP_ATTN, SP_TAP_A, SP_TAP_Y = 0, 1, 2, 3
+SP_TAP_QKV, SP_TAP_ATTN, SP_TAP_A, SP_TAP_Y, SP_TAP_X = 0, 1, 2, 3, 4
 SP_N_STAGES = 8
 STAGES = ("soft_prep", "attention", "merge", "o_proj", "post_norm", "gate_up", "down", "classifier")
 
 # Every function the header declares, with its C signature.
-EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward", "sp_probe_destroy",
-           "sp_probe_status_string", "sp_probe_tap_bytes", "sp_probe_copy_tap",
-           "sp_probe_check_device_error", "sp_probe_profile_read", "sp_probe_plan")
+EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward",
+           "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
+           "sp_probe_tap_bytes", "sp_probe_copy_tap", "sp_probe_check_device_error",
+           "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive")
 
 
 class sp_probe_config(ctypes.Structure):
@@ -55,6 +56,11 @@ class sp_probe_weights(ctypes.Structure):
                  "final_norm", "w_cls", "b_cls")]
 
 
+
+class sp_probe_fusion(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("fc_norm_hidden", "fc_norm_embed", "w_fc")]
+
+
 _lib = None
 
 
@@ -75,6 +81,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_init.restype = ctypes.c_int
     lib.sp_probe_forward.argtypes = [vp, P(sp_kv_cache), vp, vp, vp, P(sp_probe_weights), vp, vp]
     lib.sp_probe_forward.restype = ctypes.c_int
+    lib.sp_probe_forward_recursive.argtypes = [vp, P(sp_kv_cache), vp, vp, vp, vp, P(sp_probe_fusion),
+                                               P(sp_probe_weights), vp, vp]
+    lib.sp_probe_forward_recursive.restype = ctypes.c_int
     lib.sp_probe_destroy.argtypes = [vp]
     lib.sp_probe_destroy.restype = ctypes.c_int
     lib.sp_probe_status_string.argtypes = [ctypes.c_int]
@@ -89,6 +98,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_profile_read.restype = ctypes.c_int
     lib.sp_probe_plan.argtypes = [vp, ctypes.c_int32] + [P(ctypes.c_int32)] * 4
     lib.sp_probe_plan.restype = ctypes.c_int
+    lib.sp_probe_plan_recursive.argtypes = [vp, ctypes.c_int32] + [P(ctypes.c_int32)] * 4
+    lib.sp_probe_plan_recursive.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -124,6 +135,13 @@ def sp_probe_forward(h, kv: sp_kv_cache, seq_lens, block_table, soft_prompt,
                      weights: sp_probe_weights, logits, stream) -> int:
     return load().sp_probe_forward(h, ctypes.byref(kv), seq_lens, block_table, soft_prompt,
                                    ctypes.byref(weights), logits, stream)
+
+
+def sp_probe_forward_recursive(h, kv: sp_kv_cache, seq_lens, block_table, soft_prompt, hidden_last,
+                               fusion: sp_probe_fusion, weights: sp_probe_weights, logits, stream) -> int:
+    return load().sp_probe_forward_recursive(h, ctypes.byref(kv), seq_lens, block_table, soft_prompt,
+                                             hidden_last, ctypes.byref(fusion), ctypes.byref(weights),
+                                             logits, stream)
 
 
 def sp_probe_destroy(h) -> int:
@@ -168,6 +186,10 @@ def make_weights(params: dict) -> sp_probe_weights:
                                 "w_up", "w_down", "final_norm", "w_cls", "b_cls")})
 
 
+def make_fusion(fusion: dict) -> sp_probe_fusion:
+    return sp_probe_fusion(**{n: _ptr(fusion.get(n)) for n in ("fc_norm_hidden", "fc_norm_embed", "w_fc")})
+
+
 class Probe:
     """One library handle (workspace) for a workload shape."""
 
@@ -202,6 +224,24 @@ class Probe:
         _check(st, "sp_probe_forward")
         return logits
 
+    def forward_recursive(self, kv, params: dict, fusion: dict, logits=None, stream=None, batch=None):
+        """Recursive SP-k; fusion holds fc_norm_hidden, fc_norm_embed, w_fc and
+        hidden_last [B][d] (paper_2608_28099_amd.inputs.fusion_params)."""
+        import torch
+        B = kv.seq_lens.shape[0] if batch is None else batch
+        if logits is None:
+            logits = torch.empty((B, self.w.n_classes), dtype=torch.float32, device=kv.pool.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(kv.pool.device).cuda_stream
+        self._kv = make_kv(kv, B)
+        self._wt = make_weights(params)
+        self._fu = make_fusion(fusion)
+        st = sp_probe_forward_recursive(self.h, self._kv, kv.seq_lens.data_ptr(), _ptr(kv.block_table),
+                                        params["soft_prompt"].data_ptr(), _ptr(fusion["hidden_last"]),
+                                        self._fu, self._wt, logits.data_ptr(), stream)
+        _check(st, "sp_probe_forward_recursive")
+        return logits
+
     def tap(self, tap: int, batch: int, device):
         import torch
         n = self.lib.sp_probe_tap_bytes(self.h, tap, batch)
@@ -213,6 +253,13 @@ class Probe:
     def plan(self, batch: int):
         vals = [ctypes.c_int32() for _ in range(4)]
         _check(self.lib.sp_probe_plan(self.h, batch, *[ctypes.byref(v) for v in vals]), "plan")
+        return {"split_len": vals[0].value, "max_splits": vals[1].value,
+                "rows_per_kv_head": vals[2].value, "query_groups": vals[3].value}
+
+    def plan_recursive(self, batch: int):
+        vals = [ctypes.c_int32() for _ in range(4)]
+        _check(self.lib.sp_probe_plan_recursive(self.h, batch, *[ctypes.byref(v) for v in vals]),
+               "plan_recursive")
         return {"split_len": vals[0].value, "max_splits": vals[1].value,
                 "rows_per_kv_head": vals[2].value, "query_groups": vals[3].value}
 

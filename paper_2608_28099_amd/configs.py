@@ -115,3 +115,19 @@ SMALL_G5_BF16 = Workload(
     layout="paged", kv_std=1.0, seed=13, pool="mean", cls_bias=True)
 
 STRESS = {w.name: w for w in (TINY_PEAKY_F32, TINY_RAGGED_F32, SMALL_BF16, SMALL_G5_BF16)}
+
+# Recursive SP-k (the MTP input fusion of Sec. 3.1 chained over k steps,
+# Sec. 3.2) on the same head shapes, with the paper's k in {1, 2, 5}.  The
+# long-context one is the benchmark's recursive workload.
+TINY_F32_SP2 = TINY_F32.replace(name="tiny_f32_sp2", k=2, weight_std=0.1, seed=60)
+TINY_RAGGED_F32_SP5 = TINY_RAGGED_F32.replace(name="tiny_ragged_f32_sp5", k=5, seed=61)
+SMALL_BF16_SP5 = SMALL_BF16.replace(name="small_bf16_sp5", k=5, seed=62)
+SMALL_BF16_SP1 = SMALL_BF16.replace(name="small_bf16_sp1", k=1, seed=63)
+SMALL_G5_BF16_SP2 = SMALL_G5_BF16.replace(name="small_g5_bf16_sp2", k=2, seed=64)   # mean, bias
+QWEN9B_BF16_SP5 = QWEN9B_BF16.replace(name="9b_bf16_sp5", k=5)
+QWEN27B_BF16_SP2 = QWEN27B_BF16.replace(name="27b_bf16_sp2", k=2)
+LONG_9B_BF16_SP5 = LONG_9B_BF16.replace(name="long_9b_bf16_sp5", k=5)
+
+RECURSIVE = {w.name: w for w in (TINY_F32_SP2, TINY_RAGGED_F32_SP5, SMALL_BF16_SP5, SMALL_BF16_SP1,
+                                 SMALL_G5_BF16_SP2, QWEN9B_BF16_SP5, QWEN27B_BF16_SP2,
+                                 LONG_9B_BF16_SP5)}

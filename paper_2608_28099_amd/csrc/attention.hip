@@ -533,12 +533,12 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
   const int64_t base = ((int64_t)b * p.n_kv + g) * p.max_splits * p.r_alloc + r;
-  const int j = r / p.group, h = g * p.group + r % p.group;
+  const int j = p.step + r / p.group, h = g * p.group + r % p.group;
   const int i0 = lane * DPL;
 
   const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + r) * p.hd + i0;
   const int64_t ko = ((int64_t)b * p.n_kv + g) * p.ks * p.hd + i0;  // [ks][hd]
-  const int64_t vo = (int64_t)g * p.ks * p.hd + i0;                 // [ks][hd]
+  const int64_t vo = ((p.per_seq ? (int64_t)b * p.n_kv : 0) + g) * p.ks * p.hd + i0;  // [ks][hd]
   float qv[DPL];
   soft_load<TI, DPL>(p.q, p.q_lo, qo, qv);
   // soft scores in log2 units (q carries log2(e)/sqrt(hd)); lane jj keeps key jj's.

@@ -158,7 +158,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
           if (EPI == kEpiResidRow)
             v += (float)((const bf16*)p.r)[(int64_t)(m % p.r_mod) * p.N + n];
           else if (EPI == kEpiResidF32)
-            v += ((const float*)p.r)[(int64_t)m * p.ldc + n];
+            v += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
           ((float*)p.c)[(int64_t)m * p.ldc + n] = v;
         }
       }
@@ -194,7 +194,7 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   float acc = 0.f;
   for (int k = 0; k < p.K; ++k) acc += a[k] * w[k];
   if (EPI == kEpiResidRow) acc += ((const float*)p.r)[(int64_t)(m % p.r_mod) * p.N + n];
-  if (EPI == kEpiResidF32) acc += ((const float*)p.r)[(int64_t)m * p.ldc + n];
+  if (EPI == kEpiResidF32) acc += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }
 

@@ -10,24 +10,28 @@ namespace sp {
 enum DType { kF32 = 0, kBF16 = 1, kF16 = 2 };
 
 // ---------------------------------------------------------------- soft-row prep
-// out[r][i] = x[r][i] / sqrt(mean_i x[r][i]^2 + eps) * gain[i], rows r < rows.
+// out[r][i] = x[r][i] / sqrt(mean_i x[r][i]^2 + eps) * gain[i], rows r < rows
+// (row strides ld_x, ld_out in elements).  gain2 (nullable): the result is
+// normed once more with gain2 (RMSNorm(RMSNorm(x; gain); gain2)), in fp32.
 hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const void* x,
-                               const void* gain, void* out, int rows, int d, float eps,
-                               hipStream_t s);
+                               int64_t ld_x, const void* gain, const void* gain2, void* out,
+                               int64_t ld_out, int rows, int d, float eps, hipStream_t s);
 
 struct RopeParams {
-  const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32
+  const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32 ([B][k][...] when per_seq)
   const int* seq_lens;     // device [B]
   const int* err;          // nullable: skip everything if *err != 0
   void* q;                 // [B][n_kv][r_alloc][hd], scaled by q_scale
   void* k_soft;            // [B][n_kv][ks][hd] (rotated soft keys)
-  void* v_soft;            // [n_kv][ks][hd] (batch-invariant)
+  void* v_soft;            // [n_kv][ks][hd] (batch-invariant), or [B][n_kv][ks][hd] (per_seq)
   // bf16 split output (dt == kBF16): q, k_soft, v_soft receive bf16(x) and these
   // the remainders bf16(x - bf16(x)), same layouts
   void* q_lo;
   void* k_soft_lo;
   void* v_soft_lo;
   int n_q, n_kv, hd, k, group, r_alloc, ks, max_seq_len;
+  int step;                // rows j go to position N_b + step + j and soft slot step + j
+  int per_seq;             // projections and values per sequence (recursive steps)
   double rope_base;
   float q_scale;           // log2(e) / sqrt(hd)
 };
@@ -70,6 +74,8 @@ struct MergeParams {
   const void* v_soft_lo;
   void* out;               // [B k][n_q hd] (activation dtype)
   int n_kv, group, k, rows, r_alloc, hd, ks, max_splits, split_len, max_seq_len, n_q;
+  int step;                // row r is soft row step + r / group (sees soft keys 0..that row)
+  int per_seq;             // v_soft is [B][n_kv][ks][hd] instead of [n_kv][ks][hd]
 };
 // dt: storage dtype of the config (the output is fp16 for bf16 storage)
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s);
@@ -78,7 +84,7 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
 enum Epilogue {
   kEpiStore = 0,      // C fp32 = acc
   kEpiResidRow = 1,   // C fp32 = acc + R[m % r_mod][n]   (R in the storage dtype)
-  kEpiResidF32 = 2,   // C fp32 = acc + R[m][n]           (R fp32, ld = ldc)
+  kEpiResidF32 = 2,   // C fp32 = acc + R[m * r_ld + n]   (R fp32; r_ld 0 = one row for all m)
   kEpiSwiglu = 3      // C (activation dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
 };
 struct GemmParams {
@@ -89,7 +95,7 @@ struct GemmParams {
   int ldb;                 // row stride of every b[i]
   void* c;
   const void* r;           // residual
-  int M, N, K, lda, ldc, r_mod;
+  int M, N, K, lda, ldc, r_mod, r_ld;
 };
 // dt: storage dtype of the weights (kF32: fp32 VALU path; kBF16: fp16 MFMA path)
 hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s);

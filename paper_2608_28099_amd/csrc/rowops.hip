@@ -38,11 +38,12 @@ __device__ __forceinline__ void store4(T* p, const float (&v)[4]) {
 }
 
 template <typename TI, typename TG, typename TO>
-__global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, const TG* gain, TO* out, int d,
+__global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, const TG* gain,
+                                                    const TG* gain2, TO* out, int64_t ld_out, int d,
                                                     float eps) {
   __shared__ float red[4];
   const int r = blockIdx.x;
-  const TI* xr = x + (int64_t)r * d;
+  const TI* xr = x + (int64_t)r * ld_x;
   float v[kRowChunks][4];
   float ss = 0.f;
 #pragma unroll
@@ -55,26 +56,45 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, const TG* gain,
     }
   }
   ss = block_sum_256(ss, red);
-  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  TO* orow = out + (int64_t)r * d;
+  float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  // optional second norm of the result with gain2 (two RMSNorms in a row)
+  for (int pass = 0; pass < (gain2 ? 2 : 1); ++pass) {
+    const TG* g = pass ? gain2 : gain;
+    float ss2 = 0.f;
+#pragma unroll
+    for (int c = 0; c < kRowChunks; ++c) {
+      const int i = 4 * (threadIdx.x + 256 * c);
+      if (i < d) {
+        float gv[4];
+        load4(g + i, gv);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          v[c][e] = v[c][e] * inv * gv[e];
+          ss2 += v[c][e] * v[c][e];
+        }
+      }
+    }
+    if (gain2 && pass == 0) {
+      ss2 = block_sum_256(ss2, red);
+      inv = 1.0f / sqrtf(ss2 / (float)d + eps);
+    }
+  }
+  TO* orow = out + (int64_t)r * ld_out;
 #pragma unroll
   for (int c = 0; c < kRowChunks; ++c) {
     const int i = 4 * (threadIdx.x + 256 * c);
-    if (i < d) {
-      float gv[4];
-      load4(gain + i, gv);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[c][e] = v[c][e] * inv * gv[e];
-      store4(orow + i, v[c]);
-    }
+    if (i < d) store4(orow + i, v[c]);
   }
 }
 
 // ---------------------------------------------------------------- RoPE + scatter
 // One workgroup per (soft row j, sequence b): the rotation of pair (i, i + hd/2)
-// at position N_b + j by angle (N_b + j) * base^(-2i/hd) is computed once, in
-// fp64, into LDS, then applied to every query and key head of the row; the
-// value heads (no rotation, the same for every sequence) are written by b = 0.
+// at position N_b + t, t = step + j, by angle (N_b + t) * base^(-2i/hd) is
+// computed once, in fp64, into LDS, then applied to every query and key head of
+// the row, which goes to soft slot t.  The value heads are not rotated; in the
+// one-pass form (per_seq = 0) they are the same for every sequence and written
+// by b = 0, in the recursive form every sequence has its own row of
+// projections ([B][k] rows) and its own values.
 // SPLIT (T = bf16): each value x is stored as hi = bf16(x) and lo = bf16(x - hi).
 template <typename T, bool SPLIT>
 __device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
@@ -93,12 +113,13 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
   n = n < 0 ? 0 : (n > p.max_seq_len ? p.max_seq_len : n);
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     const double theta = pow(p.rope_base, -2.0 * (double)i / (double)hd);
-    const double ang = (double)(n + j) * theta;
+    const double ang = (double)(n + p.step + j) * theta;
     cs[i] = (float)cos(ang);
     sn[i] = (float)sin(ang);
   }
   __syncthreads();
-  const float* row = p.qkv + (int64_t)j * (p.n_q + 2 * p.n_kv) * hd;
+  const int slot = p.step + j;
+  const float* row = p.qkv + ((int64_t)(p.per_seq ? b * p.k : 0) + j) * (p.n_q + 2 * p.n_kv) * hd;
   const int nrot = (p.n_q + p.n_kv) * half;
   for (int e = threadIdx.x; e < nrot; e += blockDim.x) {
     const int h = e / half, i = e % half;
@@ -112,15 +133,16 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
       put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
     } else {
       const int g = h - p.n_q;
-      const int64_t base = (((int64_t)b * p.n_kv + g) * p.ks + j) * hd;
+      const int64_t base = (((int64_t)b * p.n_kv + g) * p.ks + slot) * hd;
       put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i, r0);
       put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i + half, r1);
     }
   }
-  if (b == 0) {
+  if (p.per_seq || b == 0) {
+    const int64_t vb = p.per_seq ? (int64_t)b * p.n_kv : 0;
     for (int e = threadIdx.x; e < p.n_kv * hd; e += blockDim.x) {
       const int g = e / hd, i = e % hd;
-      put<T, SPLIT>(p.v_soft, p.v_soft_lo, ((int64_t)g * p.ks + j) * hd + i, row[(p.n_q + p.n_kv + g) * hd + i]);
+      put<T, SPLIT>(p.v_soft, p.v_soft_lo, ((vb + g) * p.ks + slot) * hd + i, row[(p.n_q + p.n_kv + g) * hd + i]);
     }
   }
 }
@@ -198,17 +220,20 @@ __global__ void validate_meta(const ValidateParams p) {
 }  // namespace
 
 hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const void* x,
-                               const void* gain, void* out, int rows, int d, float eps,
-                               hipStream_t s) {
+                               int64_t ld_x, const void* gain, const void* gain2, void* out,
+                               int64_t ld_out, int rows, int d, float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
-  if (d % 4 || d > 1024 * kRowChunks) return hipErrorInvalidValue;
+  if (d % 4 || d > 1024 * kRowChunks || ld_x % 4 || ld_out % 4) return hipErrorInvalidValue;
   const dim3 grid(rows), block(256);
   if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
-    hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, (const bf16*)gain, (f16*)out, d, eps);
+    hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, ld_x,
+                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps);
   else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kF16)
-    hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16>), grid, block, 0, s, (const float*)x, (const bf16*)gain, (f16*)out, d, eps);
+    hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16>), grid, block, 0, s, (const float*)x, ld_x,
+                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps);
   else if (in_dt == kF32 && gain_dt == kF32 && out_dt == kF32)
-    hipLaunchKernelGGL((rmsnorm_rows<float, float, float>), grid, block, 0, s, (const float*)x, (const float*)gain, (float*)out, d, eps);
+    hipLaunchKernelGGL((rmsnorm_rows<float, float, float>), grid, block, 0, s, (const float*)x, ld_x,
+                       (const float*)gain, (const float*)gain2, (float*)out, ld_out, d, eps);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstring>
+#include <deque>
 #include <new>
 #include <vector>
 
@@ -18,19 +19,34 @@ namespace {
 
 using namespace sp;
 
+// Profiling: a forward records one event at its start and one after every
+// stage (the recursive forward: after every stage of every step), taken from a
+// fixed pool used as a ring; the records of the last forwards that still fit
+// are kept.
 constexpr int kMaxProfiled = 256;
-constexpr int kEventsPerForward = SP_N_STAGES + 1;
+constexpr int kEventPool = kMaxProfiled * (SP_N_STAGES + 1);
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 bool is_pow2(int64_t x) { return x > 0 && (x & (x - 1)) == 0; }
 int ilog2(int64_t x) { int r = 0; while ((int64_t(1) << r) < x) ++r; return r; }
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Attention launch shape for `rows` query rows per KV head.
+struct AttnPlan {
+  int rows, waves, n_qgroups, r_alloc, split_len, max_splits;
+};
+
 struct Plan {
   int group, rows, waves, n_qgroups, r_alloc, ks, nqkv, split_len, max_splits, esz;
+  AttnPlan rec;  // recursive steps: one soft row (G query rows) per KV head
   // workspace offsets (bytes)
   size_t off_u, off_qkv, off_q, off_ksoft, off_vsoft, off_q_lo, off_ksoft_lo, off_vsoft_lo,
-      off_opart, off_ml, off_attn, off_a, off_w, off_s, off_y, off_err, total;
+      off_opart, off_ml, off_attn, off_a, off_w, off_s, off_y, off_err;
+  // recursive steps only: per-sequence queries and soft keys/values, the fused
+  // rows and their inputs
+  size_t off_rq, off_rq_lo, off_rks, off_rks_lo, off_rvs, off_rvs_lo, off_rqkv, off_ru, off_rhn,
+      off_ren, off_rce, off_rx;
+  size_t total;
 };
 
 int check_config(const sp_probe_config* c) {
@@ -50,19 +66,25 @@ int check_config(const sp_probe_config* c) {
   if (c->hidden % mult || c->intermediate % mult) return SP_ERR_UNSUPPORTED;
   if (c->dtype == SP_F32 && c->k * (c->n_q_heads / c->n_kv_heads) > 64) return SP_ERR_UNSUPPORTED;
   if (c->hidden > 16384) return SP_ERR_UNSUPPORTED;
+  if (c->dtype == SP_BF16) {
+    // byte offsets inside one MFMA projection operand (activations [B k] rows,
+    // or one weight matrix) are 32-bit
+    const int64_t qw = (int64_t)c->n_q_heads * c->head_dim;
+    const int64_t widest = std::max<int64_t>({c->hidden, qw, c->intermediate});
+    const int64_t rows = std::max<int64_t>({(int64_t)c->max_batch * c->k, qw, c->intermediate});
+    if (rows * widest * 2 >= (int64_t(1) << 31)) return SP_ERR_UNSUPPORTED;
+  }
   return SP_OK;
 }
 
-Plan make_plan(const sp_probe_config& c) {
-  Plan p{};
-  p.esz = c.dtype == SP_BF16 ? 2 : 4;
-  p.group = c.n_q_heads / c.n_kv_heads;
-  p.rows = c.k * p.group;
-  const int tiles = (p.rows + 15) / 16;
+AttnPlan attn_plan(const sp_probe_config& c, int rows) {
+  AttnPlan a{};
+  a.rows = rows;
+  const int tiles = (rows + 15) / 16;
   if (c.dtype == SP_F32) {
-    p.waves = 0;
-    p.n_qgroups = 1;
-    p.r_alloc = p.rows;
+    a.waves = 0;
+    a.n_qgroups = 1;
+    a.r_alloc = rows;
   } else {
     // one wave per 16-row query tile, at most 8 (head_dim 128) or 16 (64) waves
     // per workgroup, whose register budget then still fits without spills; the
@@ -74,14 +96,12 @@ Plan make_plan(const sp_probe_config& c) {
     int w = max_w;
     for (int cand : kWaves)
       if (cand >= per_group) { w = cand; break; }
-    p.waves = w;
-    p.n_qgroups = (tiles + w - 1) / w;
-    p.r_alloc = p.n_qgroups * w * 16;
+    a.waves = w;
+    a.n_qgroups = (tiles + w - 1) / w;
+    a.r_alloc = a.n_qgroups * w * 16;
   }
-  p.ks = ((c.k + 31) / 32) * 32;
-  p.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
   if (c.split_len) {
-    p.split_len = c.split_len;
+    a.split_len = c.split_len;
   } else if (c.dtype == SP_BF16) {
     // Splits sized so that the attention grid at the full batch and length is
     // about one round of resident workgroups (256 compute units x 3 workgroups
@@ -89,43 +109,71 @@ Plan make_plan(const sp_probe_config& c) {
     // and a drain.  At most max_seq_len / 2 (two splits for the longest
     // sequence, so batches of mixed lengths still balance), at least 1024,
     // a multiple of 256.
-    const int64_t slots = 256 * (p.waves <= 4 ? 3 : 2);
-    const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * p.n_qgroups;
+    const int64_t slots = 256 * (a.waves <= 4 ? 3 : 2);
+    const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * a.n_qgroups;
     const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
     const int64_t half = ((int64_t)c.max_seq_len / 2 + 255) / 256 * 256;
     int64_t sl = (want + 255) / 256 * 256;
     sl = std::min(sl, half);
-    p.split_len = (int)std::max<int64_t>(sl, 1024);
+    a.split_len = (int)std::max<int64_t>(sl, 1024);
   } else {
     // fp32 path: at most 8 splits per sequence, between 1024 and 16384 tokens each
     int sl = 1024;
     while (sl < 16384 && (int64_t)sl * 8 < c.max_seq_len) sl *= 2;
-    p.split_len = sl;
+    a.split_len = sl;
   }
-  p.max_splits = c.max_seq_len > 0 ? (c.max_seq_len + p.split_len - 1) / p.split_len : 1;
+  a.max_splits = c.max_seq_len > 0 ? (c.max_seq_len + a.split_len - 1) / a.split_len : 1;
+  return a;
+}
+
+Plan make_plan(const sp_probe_config& c) {
+  Plan p{};
+  p.esz = c.dtype == SP_BF16 ? 2 : 4;
+  p.group = c.n_q_heads / c.n_kv_heads;
+  const AttnPlan one = attn_plan(c, c.k * p.group);
+  p.rows = one.rows; p.waves = one.waves; p.n_qgroups = one.n_qgroups; p.r_alloc = one.r_alloc;
+  p.split_len = one.split_len; p.max_splits = one.max_splits;
+  p.rec = attn_plan(c, p.group);
+  p.ks = ((c.k + 31) / 32) * 32;
+  p.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
 
   const size_t B = (size_t)c.max_batch, M = B * c.k, d = c.hidden, hd = c.head_dim;
-  const size_t e = p.esz;
+  const size_t kv = (size_t)c.n_kv_heads, e = p.esz;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align256(o + bytes); return at; };
   p.off_u = take((size_t)c.k * d * e);
   p.off_qkv = take((size_t)c.k * p.nqkv * 4);
-  p.off_q = take(B * c.n_kv_heads * p.r_alloc * hd * e);
-  p.off_ksoft = take(B * c.n_kv_heads * p.ks * hd * e);
-  p.off_vsoft = take((size_t)c.n_kv_heads * hd * p.ks * e);
+  p.off_q = take(B * kv * p.r_alloc * hd * e);
+  p.off_ksoft = take(B * kv * p.ks * hd * e);
+  p.off_vsoft = take(kv * hd * p.ks * e);
   // remainders of the split bf16 queries and soft keys/values (bf16 storage only)
   const size_t lo = c.dtype == SP_BF16 ? 1 : 0;
-  p.off_q_lo = take(lo * B * c.n_kv_heads * p.r_alloc * hd * e);
-  p.off_ksoft_lo = take(lo * B * c.n_kv_heads * p.ks * hd * e);
-  p.off_vsoft_lo = take(lo * (size_t)c.n_kv_heads * hd * p.ks * e);
-  p.off_opart = take(B * c.n_kv_heads * p.max_splits * p.r_alloc * hd * 4);
-  p.off_ml = take(B * c.n_kv_heads * p.max_splits * p.r_alloc * 8);
+  p.off_q_lo = take(lo * B * kv * p.r_alloc * hd * e);
+  p.off_ksoft_lo = take(lo * B * kv * p.ks * hd * e);
+  p.off_vsoft_lo = take(lo * kv * hd * p.ks * e);
+  // split partials: shared by the one-pass and the recursive forwards
+  const size_t part_rows = std::max((size_t)p.max_splits * p.r_alloc,
+                                    (size_t)p.rec.max_splits * p.rec.r_alloc);
+  p.off_opart = take(B * kv * part_rows * hd * 4);
+  p.off_ml = take(B * kv * part_rows * 8);
   p.off_attn = take(M * c.n_q_heads * hd * e);
   p.off_a = take(M * d * 4);
   p.off_w = take(M * d * e);
   p.off_s = take(M * (size_t)c.intermediate * e);
   p.off_y = take(M * d * 4);
   p.off_err = take(256);
+  p.off_rq = take(B * kv * p.rec.r_alloc * hd * e);
+  p.off_rq_lo = take(lo * B * kv * p.rec.r_alloc * hd * e);
+  p.off_rks = take(B * kv * p.ks * hd * e);
+  p.off_rks_lo = take(lo * B * kv * p.ks * hd * e);
+  p.off_rvs = take(B * kv * p.ks * hd * e);
+  p.off_rvs_lo = take(lo * B * kv * p.ks * hd * e);
+  p.off_rqkv = take(B * p.nqkv * 4);
+  p.off_ru = take(B * d * e);
+  p.off_rhn = take(B * d * e);
+  p.off_ren = take((size_t)c.k * d * e);
+  p.off_rce = take((size_t)c.k * d * 4);
+  p.off_rx = take(M * d * 4);
   p.total = o;
   return p;
 }
@@ -137,8 +185,10 @@ struct sp_probe {
   Plan plan;
   int device;
   char* ws;
-  std::vector<hipEvent_t> events;  // kMaxProfiled * kEventsPerForward, used as a ring
-  int64_t n_profiled;
+  std::vector<hipEvent_t> events;  // kEventPool events (profiling mode), used as a ring
+  struct Record { int start, marks; };
+  std::deque<Record> records;      // forwards whose events are still in the pool, oldest first
+  int cursor;                      // next free event of the pool
 };
 
 namespace {
@@ -154,6 +204,118 @@ int check_device() {
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return SP_ERR_NO_DEVICE;
   if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0) return SP_ERR_NO_DEVICE;
   return SP_OK;
+}
+
+// Events for a forward of `marks` marks (contiguous in the pool; the oldest
+// records they overlap are dropped).  nullptr when profiling is off.
+hipEvent_t* prof_begin(sp_probe* h, int marks) {
+  if (h->events.empty() || marks > kEventPool) return nullptr;
+  if (h->cursor + marks > kEventPool) h->cursor = 0;
+  const int lo = h->cursor, hi = h->cursor + marks;
+  while (!h->records.empty()) {
+    const sp_probe::Record& r = h->records.front();
+    if (r.start < hi && r.start + r.marks > lo) h->records.pop_front();
+    else break;
+  }
+  return &h->events[lo];
+}
+
+void prof_commit(sp_probe* h, int marks) {
+  h->records.push_back({h->cursor, marks});
+  h->cursor += marks;
+}
+
+// Host-side checks shared by the forwards; *noop is set for an empty batch.
+int check_forward(const sp_probe* h, const sp_kv_cache* kv, const int32_t* seq_lens,
+                  const int32_t* block_table, const void* soft_prompt, const sp_probe_weights* wt,
+                  const float* logits, bool* noop) {
+  *noop = false;
+  if (!h || !kv || !wt) return SP_ERR_INVALID_ARG;
+  const sp_probe_config& c = h->cfg;
+  const int B = kv->batch;
+  if (B < 0) return SP_ERR_INVALID_ARG;
+  if (B > c.max_batch) return SP_ERR_CAPACITY;
+  if (B == 0) { *noop = true; return SP_OK; }
+  if (!seq_lens || !soft_prompt || !logits) return SP_ERR_INVALID_ARG;
+  const void* wptr[11] = {wt->in_norm, wt->w_q, wt->w_k, wt->w_v, wt->w_o, wt->post_norm,
+                          wt->w_gate, wt->w_up, wt->w_down, wt->final_norm, wt->w_cls};
+  for (const void* q : wptr)
+    if (!q || !aligned16(q)) return SP_ERR_INVALID_ARG;
+  if (!aligned16(soft_prompt)) return SP_ERR_INVALID_ARG;
+  if (!kv->k_base || !kv->v_base || !aligned16(kv->k_base) || !aligned16(kv->v_base))
+    return SP_ERR_INVALID_ARG;
+  if (kv->block_size < 16 || !is_pow2(kv->block_size) || kv->max_blocks_per_seq < 1 ||
+      kv->num_blocks < 1)
+    return SP_ERR_INVALID_ARG;
+  const int64_t tile = (int64_t)kv->block_size * c.head_dim;  // elements of one K or V tile
+  const int64_t vec = 16 / h->plan.esz;
+  if (kv->k_stride_block % vec || kv->k_stride_head % vec || kv->v_stride_block % vec ||
+      kv->v_stride_head % vec || kv->k_stride_block < 0 || kv->v_stride_block < 0 ||
+      kv->k_stride_head < tile || kv->v_stride_head < tile)
+    return SP_ERR_INVALID_ARG;
+  if ((int64_t)kv->max_blocks_per_seq * kv->block_size < (int64_t)c.max_seq_len)
+    return SP_ERR_INVALID_ARG;  // a sequence of max_seq_len tokens must fit in a table row
+  if (!block_table && (int64_t)B * kv->max_blocks_per_seq > kv->num_blocks) return SP_ERR_INVALID_ARG;
+  return SP_OK;
+}
+
+// Split-attention parameters over the caller's cache for one attention plan.
+AttnParams attn_params(const sp_probe_config& c, const AttnPlan& a, const sp_kv_cache* kv,
+                       const int32_t* seq_lens, const int32_t* block_table, const int* errp,
+                       const void* q, const void* q_lo, float* o_part, float2* ml_part) {
+  AttnParams ap{};
+  ap.q = q;
+  ap.q_lo = q_lo;
+  ap.k_base = kv->k_base; ap.v_base = kv->v_base;
+  ap.k_sb = kv->k_stride_block; ap.k_sh = kv->k_stride_head;
+  ap.v_sb = kv->v_stride_block; ap.v_sh = kv->v_stride_head;
+  ap.block_table = block_table;
+  ap.seq_lens = seq_lens;
+  ap.err = errp;
+  ap.o_part = o_part;
+  ap.ml_part = ml_part;
+  ap.n_kv = c.n_kv_heads; ap.rows = a.rows;
+  ap.r_alloc = a.r_alloc; ap.n_qgroups = a.n_qgroups;
+  ap.bs_log2 = ilog2(kv->block_size); ap.mbps = kv->max_blocks_per_seq;
+  ap.max_seq_len = c.max_seq_len; ap.split_len = a.split_len; ap.max_splits = a.max_splits;
+  return ap;
+}
+
+GemmParams gemm_one(const void* a, int lda, const void* w, int ldb, void* c, int ldc, int M, int N,
+                    int K) {
+  GemmParams g{};
+  g.a = a;
+  g.b[0] = g.b[1] = g.b[2] = w;
+  g.b_split0 = g.b_split1 = N;
+  g.ldb = ldb;
+  g.c = c;
+  g.M = M; g.N = N; g.K = K; g.lda = lda; g.ldc = ldc;
+  return g;
+}
+
+GemmParams gemm_qkv(const sp_probe_config& c, const Plan& pl, const sp_probe_weights* wt,
+                    const void* a, void* out, int M) {
+  GemmParams g{};
+  g.a = a;
+  g.b[0] = wt->w_q; g.b[1] = wt->w_k; g.b[2] = wt->w_v;
+  g.b_split0 = c.n_q_heads * c.head_dim;
+  g.b_split1 = (c.n_q_heads + c.n_kv_heads) * c.head_dim;
+  g.ldb = c.hidden;
+  g.c = out;
+  g.M = M; g.N = pl.nqkv; g.K = c.hidden; g.lda = c.hidden; g.ldc = pl.nqkv;
+  return g;
+}
+
+GemmParams gemm_gate_up(const sp_probe_config& c, const sp_probe_weights* wt, const void* a,
+                        void* out, int M) {
+  GemmParams g{};
+  g.a = a;
+  g.b[0] = wt->w_gate; g.b[1] = wt->w_up; g.b[2] = wt->w_up;
+  g.b_split0 = g.b_split1 = 2 * c.intermediate;
+  g.ldb = c.hidden;
+  g.c = out;
+  g.M = M; g.N = 2 * c.intermediate; g.K = c.hidden; g.lda = c.hidden; g.ldc = c.intermediate;
+  return g;
 }
 
 }  // namespace
@@ -188,7 +350,7 @@ SP_API int sp_probe_init(const sp_probe_config* cfg, sp_probe_t** out) {
   if (!h) return SP_ERR_OUT_OF_MEMORY;
   h->cfg = *cfg;
   h->plan = make_plan(*cfg);
-  h->n_profiled = 0;
+  h->cursor = 0;
   h->ws = nullptr;
   if (hipGetDevice(&h->device) != hipSuccess) { delete h; return SP_ERR_HIP; }
   if (hipMalloc(&h->ws, h->plan.total) != hipSuccess) { delete h; return SP_ERR_OUT_OF_MEMORY; }
@@ -200,7 +362,7 @@ SP_API int sp_probe_init(const sp_probe_config* cfg, sp_probe_t** out) {
     return SP_ERR_HIP;
   }
   if (cfg->flags & SP_FLAG_PROFILE) {
-    h->events.resize((size_t)kMaxProfiled * kEventsPerForward);
+    h->events.resize(kEventPool);
     for (auto& ev : h->events) {
       if (hipEventCreate(&ev) != hipSuccess) {
         ev = nullptr;
@@ -234,51 +396,41 @@ SP_API int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len,
   return SP_OK;
 }
 
+SP_API int sp_probe_plan_recursive(const sp_probe_t* h, int32_t batch, int32_t* split_len,
+                                   int32_t* max_splits, int32_t* rows_per_kv_head,
+                                   int32_t* query_groups) {
+  if (!h || batch < 0) return SP_ERR_INVALID_ARG;
+  if (split_len) *split_len = h->plan.rec.split_len;
+  if (max_splits) *max_splits = h->plan.rec.max_splits;
+  if (rows_per_kv_head) *rows_per_kv_head = h->plan.rec.rows;
+  if (query_groups) *query_groups = h->plan.rec.n_qgroups;
+  return SP_OK;
+}
+
+#define SP_TRY(expr) do { if ((expr) != hipSuccess) return SP_ERR_HIP; } while (0)
+
 SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
                             const int32_t* block_table, const void* soft_prompt,
                             const sp_probe_weights* wt, float* logits, void* stream) {
   // ---- host-side checks: nothing is enqueued unless all pass
-  if (!h || !kv || !wt) return SP_ERR_INVALID_ARG;
+  bool noop = false;
+  const int chk = check_forward(h, kv, seq_lens, block_table, soft_prompt, wt, logits, &noop);
+  if (chk != SP_OK || noop) return chk;
   const sp_probe_config& c = h->cfg;
   const Plan& pl = h->plan;
   const int B = kv->batch;
-  if (B < 0) return SP_ERR_INVALID_ARG;
-  if (B > c.max_batch) return SP_ERR_CAPACITY;
-  if (B == 0) return SP_OK;
-  if (!seq_lens || !soft_prompt || !logits) return SP_ERR_INVALID_ARG;
-  const void* wptr[11] = {wt->in_norm, wt->w_q, wt->w_k, wt->w_v, wt->w_o, wt->post_norm,
-                          wt->w_gate, wt->w_up, wt->w_down, wt->final_norm, wt->w_cls};
-  for (const void* q : wptr)
-    if (!q || !aligned16(q)) return SP_ERR_INVALID_ARG;
-  if (!aligned16(soft_prompt)) return SP_ERR_INVALID_ARG;
-  if (!kv->k_base || !kv->v_base || !aligned16(kv->k_base) || !aligned16(kv->v_base))
-    return SP_ERR_INVALID_ARG;
-  if (kv->block_size < 16 || !is_pow2(kv->block_size) || kv->max_blocks_per_seq < 1 ||
-      kv->num_blocks < 1)
-    return SP_ERR_INVALID_ARG;
-  const int64_t tile = (int64_t)kv->block_size * c.head_dim;  // elements of one K or V tile
-  const int64_t vec = 16 / pl.esz;
-  if (kv->k_stride_block % vec || kv->k_stride_head % vec || kv->v_stride_block % vec ||
-      kv->v_stride_head % vec || kv->k_stride_block < 0 || kv->v_stride_block < 0 ||
-      kv->k_stride_head < tile || kv->v_stride_head < tile)
-    return SP_ERR_INVALID_ARG;
-  if ((int64_t)kv->max_blocks_per_seq * kv->block_size < (int64_t)c.max_seq_len)
-    return SP_ERR_INVALID_ARG;  // a sequence of max_seq_len tokens must fit in a table row
-  if (!block_table && (int64_t)B * kv->max_blocks_per_seq > kv->num_blocks) return SP_ERR_INVALID_ARG;
 
   hipStream_t s = (hipStream_t)stream;
   const DType dt = c.dtype == SP_BF16 ? kBF16 : kF32;   // storage: weights, soft prompt, KV
   const DType at_dt = c.dtype == SP_BF16 ? kF16 : kF32;  // activations feeding the MFMAs
   const int d = c.hidden, hd = c.head_dim, I = c.intermediate, M = B * c.k;
   const bool debug = c.flags & SP_FLAG_DEBUG;
-  const bool prof = c.flags & SP_FLAG_PROFILE;
   int* err = at<int>(h, pl.off_err);
   const int* errp = debug ? err : nullptr;
-  hipEvent_t* ev = nullptr;
-  if (prof) ev = &h->events[(size_t)(h->n_profiled % kMaxProfiled) * kEventsPerForward];
+  const int marks = SP_N_STAGES + 1;
+  hipEvent_t* ev = prof_begin(h, marks);
   int stage = 0;
-  auto mark = [&]() -> bool { return !prof || hipEventRecord(ev[stage++], s) == hipSuccess; };
-#define SP_TRY(expr) do { if ((expr) != hipSuccess) return SP_ERR_HIP; } while (0)
+  auto mark = [&]() -> bool { return !ev || hipEventRecord(ev[stage++], s) == hipSuccess; };
 
   if (debug) {
     ValidateParams vp{seq_lens, block_table, err, kv->num_blocks, kv->max_blocks_per_seq,
@@ -288,19 +440,9 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   if (!mark()) return SP_ERR_HIP;
 
   // stage 0: soft rows — RMSNorm, Q/K/V on the k distinct rows, RoPE per sequence
-  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, wt->in_norm, at<void>(h, pl.off_u), c.k, d,
-                             c.rms_eps, s));
-  {
-    GemmParams g{};
-    g.a = at<void>(h, pl.off_u);
-    g.b[0] = wt->w_q; g.b[1] = wt->w_k; g.b[2] = wt->w_v;
-    g.b_split0 = c.n_q_heads * hd;
-    g.b_split1 = (c.n_q_heads + c.n_kv_heads) * hd;
-    g.ldb = d;
-    g.c = at<void>(h, pl.off_qkv);
-    g.M = c.k; g.N = pl.nqkv; g.K = d; g.lda = d; g.ldc = pl.nqkv;
-    SP_TRY(launch_gemm(dt, kEpiStore, g, s));
-  }
+  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, d, wt->in_norm, nullptr,
+                             at<void>(h, pl.off_u), d, c.k, d, c.rms_eps, s));
+  SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_u), at<void>(h, pl.off_qkv), c.k), s));
   {
     RopeParams r{};
     r.qkv = at<float>(h, pl.off_qkv);
@@ -314,35 +456,25 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     r.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
     r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = c.k; r.group = pl.group;
     r.r_alloc = pl.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
+    r.step = 0; r.per_seq = 0;
     r.rope_base = c.rope_base;
     r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
     SP_TRY(launch_rope_scatter(dt, r, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 1: split attention over [cached K/V ; soft K/V]
-  AttnParams ap{};
-  ap.q = at<void>(h, pl.off_q);
-  ap.q_lo = at<void>(h, pl.off_q_lo);
-  ap.k_base = kv->k_base; ap.v_base = kv->v_base;
-  ap.k_sb = kv->k_stride_block; ap.k_sh = kv->k_stride_head;
-  ap.v_sb = kv->v_stride_block; ap.v_sh = kv->v_stride_head;
-  ap.block_table = block_table;
-  ap.seq_lens = seq_lens;
-  ap.err = errp;
-  ap.o_part = at<float>(h, pl.off_opart);
-  ap.ml_part = at<float2>(h, pl.off_ml);
-  ap.n_kv = c.n_kv_heads; ap.rows = pl.rows;
-  ap.r_alloc = pl.r_alloc; ap.n_qgroups = pl.n_qgroups;
-  ap.bs_log2 = ilog2(kv->block_size); ap.mbps = kv->max_blocks_per_seq;
-  ap.max_seq_len = c.max_seq_len; ap.split_len = pl.split_len; ap.max_splits = pl.max_splits;
+  // stage 1: split attention over the cached K/V
+  const AttnPlan one{pl.rows, pl.waves, pl.n_qgroups, pl.r_alloc, pl.split_len, pl.max_splits};
+  const AttnParams ap = attn_params(c, one, kv, seq_lens, block_table, errp, at<void>(h, pl.off_q),
+                                    at<void>(h, pl.off_q_lo), at<float>(h, pl.off_opart),
+                                    at<float2>(h, pl.off_ml));
   if (dt == kBF16)
     SP_TRY(launch_attention_bf16(ap, hd, pl.waves, B, s));
   else
     SP_TRY(launch_attention_f32(ap, hd, B, s));
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 2: merge the splits into the attention output rows b*k + j
+  // stage 2: merge the splits and the soft keys into the attention output rows b*k + j
   {
     MergeParams mp{};
     mp.o_part = ap.o_part; mp.ml_part = ap.ml_part; mp.seq_lens = seq_lens; mp.err = errp;
@@ -353,52 +485,33 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.k = c.k; mp.rows = pl.rows;
     mp.r_alloc = pl.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = pl.max_splits;
     mp.split_len = pl.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
+    mp.step = 0; mp.per_seq = 0;
     SP_TRY(launch_merge(dt, mp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
   // stage 3: a = x_j + W_o o
   {
-    GemmParams g{};
-    g.a = at<void>(h, pl.off_attn);
-    g.b[0] = g.b[1] = g.b[2] = wt->w_o;
-    g.b_split0 = g.b_split1 = d;
-    g.ldb = c.n_q_heads * hd;
-    g.c = at<void>(h, pl.off_a);
+    const int qw = c.n_q_heads * hd;
+    GemmParams g = gemm_one(at<void>(h, pl.off_attn), qw, wt->w_o, qw, at<void>(h, pl.off_a), d, M, d, qw);
     g.r = soft_prompt; g.r_mod = c.k;
-    g.M = M; g.N = d; g.K = c.n_q_heads * hd; g.lda = c.n_q_heads * hd; g.ldc = d;
     SP_TRY(launch_gemm(dt, kEpiResidRow, g, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
   // stage 4: w = RMSNorm(a; gamma_post)
-  SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, at<void>(h, pl.off_a), wt->post_norm,
-                             at<void>(h, pl.off_w), M, d, c.rms_eps, s));
+  SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, at<void>(h, pl.off_a), d, wt->post_norm, nullptr,
+                             at<void>(h, pl.off_w), d, M, d, c.rms_eps, s));
   if (!mark()) return SP_ERR_HIP;
 
   // stage 5: s = silu(W_gate w) * (W_up w)
-  {
-    GemmParams g{};
-    g.a = at<void>(h, pl.off_w);
-    g.b[0] = wt->w_gate; g.b[1] = wt->w_up; g.b[2] = wt->w_up;
-    g.b_split0 = g.b_split1 = 2 * I;
-    g.ldb = d;
-    g.c = at<void>(h, pl.off_s);
-    g.M = M; g.N = 2 * I; g.K = d; g.lda = d; g.ldc = I;
-    SP_TRY(launch_gemm(dt, kEpiSwiglu, g, s));
-  }
+  SP_TRY(launch_gemm(dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), M), s));
   if (!mark()) return SP_ERR_HIP;
 
   // stage 6: y = a + W_down s
   {
-    GemmParams g{};
-    g.a = at<void>(h, pl.off_s);
-    g.b[0] = g.b[1] = g.b[2] = wt->w_down;
-    g.b_split0 = g.b_split1 = d;
-    g.ldb = I;
-    g.c = at<void>(h, pl.off_y);
-    g.r = at<void>(h, pl.off_a);
-    g.M = M; g.N = d; g.K = I; g.lda = I; g.ldc = d;
+    GemmParams g = gemm_one(at<void>(h, pl.off_s), I, wt->w_down, I, at<void>(h, pl.off_y), d, M, d, I);
+    g.r = at<void>(h, pl.off_a); g.r_ld = d;
     SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
   }
   if (!mark()) return SP_ERR_HIP;
@@ -414,10 +527,171 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     SP_TRY(launch_final_classifier(dt, cp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
-#undef SP_TRY
-  if (prof) ++h->n_profiled;
+  if (ev) prof_commit(h, marks);
   return SP_OK;
 }
+
+SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
+                                      const int32_t* block_table, const void* soft_prompt,
+                                      const void* hidden_last, const sp_probe_fusion* fusion,
+                                      const sp_probe_weights* wt, float* logits, void* stream) {
+  // ---- host-side checks: nothing is enqueued unless all pass
+  bool noop = false;
+  const int chk = check_forward(h, kv, seq_lens, block_table, soft_prompt, wt, logits, &noop);
+  if (chk != SP_OK || noop) return chk;
+  if (!fusion || !hidden_last || !aligned16(hidden_last)) return SP_ERR_INVALID_ARG;
+  const void* fptr[3] = {fusion->fc_norm_hidden, fusion->fc_norm_embed, fusion->w_fc};
+  for (const void* q : fptr)
+    if (!q || !aligned16(q)) return SP_ERR_INVALID_ARG;
+  const sp_probe_config& c = h->cfg;
+  const Plan& pl = h->plan;
+  const AttnPlan& rp = pl.rec;
+  const int B = kv->batch, K = c.k;
+
+  hipStream_t s = (hipStream_t)stream;
+  const DType dt = c.dtype == SP_BF16 ? kBF16 : kF32;
+  const DType at_dt = c.dtype == SP_BF16 ? kF16 : kF32;
+  const int d = c.hidden, hd = c.head_dim, I = c.intermediate, qw = c.n_q_heads * hd;
+  const size_t esz = pl.esz;  // bytes of a storage element and of an activation element
+  const int64_t ld_steps = (int64_t)K * d;  // row stride of the [B][k][d] step buffers
+  const bool debug = c.flags & SP_FLAG_DEBUG;
+  int* err = at<int>(h, pl.off_err);
+  const int* errp = debug ? err : nullptr;
+  const int marks = SP_N_STAGES * K + 1;
+  hipEvent_t* ev = prof_begin(h, marks);
+  int mk = 0;
+  auto mark = [&]() -> bool { return !ev || hipEventRecord(ev[mk++], s) == hipSuccess; };
+
+  char* x_all = at<char>(h, pl.off_rx);   // fused rows x_t: fp32 [B][k][d]
+  char* a_all = at<char>(h, pl.off_a);    // a_t: fp32 [B][k][d]
+  char* y_all = at<char>(h, pl.off_y);    // y_t: fp32 [B][k][d]
+  char* o_all = at<char>(h, pl.off_attn); // attention output: [B][k][n_q hd]
+  void* hn = at<void>(h, pl.off_rhn);     // RMSNorm of the hidden state entering a step
+  const void* w_fc_embed = (const char*)fusion->w_fc + (size_t)d * esz;  // columns d..2d-1
+
+  if (debug) {
+    ValidateParams vp{seq_lens, block_table, err, kv->num_blocks, kv->max_blocks_per_seq,
+                      ilog2(kv->block_size), c.max_seq_len};
+    SP_TRY(launch_validate(vp, B, s));
+  }
+  if (!mark()) return SP_ERR_HIP;
+
+  // The soft-prompt half of the fusion does not depend on the sequence:
+  // c_t = W_fc[:, d:] RMSNorm(e_t; gamma_e) for the k steps, once.
+  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, d, fusion->fc_norm_embed, nullptr,
+                             at<void>(h, pl.off_ren), d, K, d, c.rms_eps, s));
+  SP_TRY(launch_gemm(dt, kEpiStore, gemm_one(at<void>(h, pl.off_ren), d, w_fc_embed, 2 * d,
+                                             at<void>(h, pl.off_rce), d, K, d, d), s));
+  // the first step's hidden state is the base model's last one
+  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, hidden_last, d, fusion->fc_norm_hidden, nullptr, hn, d,
+                             B, d, c.rms_eps, s));
+
+  for (int t = 0; t < K; ++t) {
+    // stage 0: x_t = W_fc[:, :d] RMSNorm(h; gamma_h) + c_t, its RMSNorm, Q/K/V, RoPE at N_b + t
+    {
+      GemmParams g = gemm_one(hn, d, fusion->w_fc, 2 * d, x_all + (size_t)t * d * 4, (int)ld_steps,
+                              B, d, d);
+      g.r = at<char>(h, pl.off_rce) + (size_t)t * d * 4; g.r_ld = 0;
+      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+    }
+    SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, x_all + (size_t)t * d * 4, ld_steps, wt->in_norm,
+                               nullptr, at<void>(h, pl.off_ru), d, B, d, c.rms_eps, s));
+    SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_ru), at<void>(h, pl.off_rqkv), B), s));
+    {
+      RopeParams r{};
+      r.qkv = at<float>(h, pl.off_rqkv);
+      r.seq_lens = seq_lens;
+      r.err = errp;
+      r.q = at<void>(h, pl.off_rq);
+      r.k_soft = at<void>(h, pl.off_rks);
+      r.v_soft = at<void>(h, pl.off_rvs);
+      r.q_lo = at<void>(h, pl.off_rq_lo);
+      r.k_soft_lo = at<void>(h, pl.off_rks_lo);
+      r.v_soft_lo = at<void>(h, pl.off_rvs_lo);
+      r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = 1; r.group = pl.group;
+      r.r_alloc = rp.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
+      r.step = t; r.per_seq = 1;
+      r.rope_base = c.rope_base;
+      r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
+      SP_TRY(launch_rope_scatter(dt, r, B, s));
+    }
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 1: split attention of the step's G query rows per KV head over the cache
+    const AttnParams ap = attn_params(c, rp, kv, seq_lens, block_table, errp, at<void>(h, pl.off_rq),
+                                      at<void>(h, pl.off_rq_lo), at<float>(h, pl.off_opart),
+                                      at<float2>(h, pl.off_ml));
+    if (dt == kBF16)
+      SP_TRY(launch_attention_bf16(ap, hd, rp.waves, B, s));
+    else
+      SP_TRY(launch_attention_f32(ap, hd, B, s));
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 2: merge with the soft keys of steps 0..t into attention rows b*k + t
+    {
+      MergeParams mp{};
+      mp.o_part = ap.o_part; mp.ml_part = ap.ml_part; mp.seq_lens = seq_lens; mp.err = errp;
+      mp.q = ap.q; mp.q_lo = ap.q_lo;
+      mp.k_soft = at<void>(h, pl.off_rks); mp.k_soft_lo = at<void>(h, pl.off_rks_lo);
+      mp.v_soft = at<void>(h, pl.off_rvs); mp.v_soft_lo = at<void>(h, pl.off_rvs_lo);
+      mp.out = o_all;
+      mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.k = K; mp.rows = rp.rows;
+      mp.r_alloc = rp.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = rp.max_splits;
+      mp.split_len = rp.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
+      mp.step = t; mp.per_seq = 1;
+      SP_TRY(launch_merge(dt, mp, B, s));
+    }
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 3: a_t = x_t + W_o o_t
+    {
+      GemmParams g = gemm_one(o_all + (size_t)t * qw * esz, K * qw, wt->w_o, qw,
+                              a_all + (size_t)t * d * 4, (int)ld_steps, B, d, qw);
+      g.r = x_all + (size_t)t * d * 4; g.r_ld = (int)ld_steps;
+      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+    }
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 4: w = RMSNorm(a_t; gamma_post)
+    SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, a_all + (size_t)t * d * 4, ld_steps, wt->post_norm,
+                               nullptr, at<void>(h, pl.off_w), d, B, d, c.rms_eps, s));
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 5: s = silu(W_gate w) * (W_up w)
+    SP_TRY(launch_gemm(dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), B), s));
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 6: y_t = a_t + W_down s
+    {
+      GemmParams g = gemm_one(at<void>(h, pl.off_s), I, wt->w_down, I, y_all + (size_t)t * d * 4,
+                              (int)ld_steps, B, d, I);
+      g.r = a_all + (size_t)t * d * 4; g.r_ld = (int)ld_steps;
+      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+    }
+    if (!mark()) return SP_ERR_HIP;
+
+    // stage 7: the step's output f_t = RMSNorm(y_t; gamma_final) is the next
+    // step's hidden state, which enters it as RMSNorm(f_t; gamma_h); after the
+    // last step, the read-out and the classifier
+    if (t + 1 < K) {
+      SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, y_all + (size_t)t * d * 4, ld_steps, wt->final_norm,
+                                 fusion->fc_norm_hidden, hn, d, B, d, c.rms_eps, s));
+    } else {
+      ClsParams cp{};
+      cp.y = (const float*)y_all;
+      cp.final_norm = wt->final_norm; cp.w_cls = wt->w_cls; cp.b_cls = wt->b_cls;
+      cp.logits = logits;
+      cp.k = K; cp.d = d; cp.n_classes = c.n_classes; cp.pool_mean = c.pool == SP_POOL_MEAN;
+      cp.eps = c.rms_eps;
+      SP_TRY(launch_final_classifier(dt, cp, B, s));
+    }
+    if (!mark()) return SP_ERR_HIP;
+  }
+  if (ev) prof_commit(h, marks);
+  return SP_OK;
+}
+
+#undef SP_TRY
 
 SP_API size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch) {
   if (!h || batch < 0 || batch > h->cfg.max_batch) return 0;
@@ -428,6 +702,7 @@ SP_API size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch) {
     case SP_TAP_ATTN: return M * c.n_q_heads * c.head_dim * e;
     case SP_TAP_A: return M * c.hidden * 4;
     case SP_TAP_Y: return M * c.hidden * 4;
+    case SP_TAP_X: return M * c.hidden * 4;
   }
   return 0;
 }
@@ -442,6 +717,7 @@ SP_API int sp_probe_copy_tap(sp_probe_t* h, int tap, int32_t batch, void* dst, s
     case SP_TAP_ATTN: off = h->plan.off_attn; break;
     case SP_TAP_A: off = h->plan.off_a; break;
     case SP_TAP_Y: off = h->plan.off_y; break;
+    case SP_TAP_X: off = h->plan.off_rx; break;
   }
   if (hipMemcpyAsync(dst, h->ws + off, n, hipMemcpyDeviceToDevice, (hipStream_t)stream) != hipSuccess)
     return SP_ERR_HIP;
@@ -468,18 +744,19 @@ SP_API int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stage
   if (!h || !stage_ms || n_stages < 1 || n_stages > SP_N_STAGES) return SP_ERR_INVALID_ARG;
   if (!(h->cfg.flags & SP_FLAG_PROFILE)) return SP_ERR_INVALID_ARG;
   for (int i = 0; i < n_stages; ++i) stage_ms[i] = 0.f;
-  const int64_t total = h->n_profiled;
-  const int64_t count = total < kMaxProfiled ? total : kMaxProfiled;
-  for (int64_t f = total - count; f < total; ++f) {
-    hipEvent_t* ev = &h->events[(size_t)(f % kMaxProfiled) * kEventsPerForward];
-    if (hipEventSynchronize(ev[SP_N_STAGES]) != hipSuccess) return SP_ERR_HIP;
-    for (int i = 0; i < n_stages; ++i) {
+  for (const sp_probe::Record& r : h->records) {
+    hipEvent_t* ev = &h->events[r.start];
+    if (hipEventSynchronize(ev[r.marks - 1]) != hipSuccess) return SP_ERR_HIP;
+    for (int i = 0; i + 1 < r.marks; ++i) {
+      const int st = i % SP_N_STAGES;
+      if (st >= n_stages) continue;
       float ms = 0.f;
       if (hipEventElapsedTime(&ms, ev[i], ev[i + 1]) != hipSuccess) return SP_ERR_HIP;
-      stage_ms[i] += ms;
+      stage_ms[st] += ms;
     }
   }
-  if (n_forwards) *n_forwards = (int32_t)count;
-  h->n_profiled = 0;
+  if (n_forwards) *n_forwards = (int32_t)h->records.size();
+  h->records.clear();
+  h->cursor = 0;
   return SP_OK;
 }

@@ -32,7 +32,8 @@ from .configs import Workload
 _TAGS = {
     "seq_len": 1, "perm": 2, "kv": 3, "soft": 10, "in_norm": 11, "w_q": 12, "w_k": 13, "w_v": 14,
     "w_o": 15, "post_norm": 16, "w_gate": 17, "w_up": 18, "w_down": 19, "final_norm": 20,
-    "w_cls": 21, "b_cls": 22,
+    "w_cls": 21, "b_cls": 22, "fc_norm_hidden": 23, "fc_norm_embed": 24, "w_fc": 25,
+    "hidden_last": 26,
 }
 
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
@@ -104,6 +105,21 @@ def params(w: Workload, device="cpu") -> dict:
                   if w.cls_bias else None),
     }
     return p
+
+
+def fusion_params(w: Workload, device="cpu") -> dict:
+    """Inputs of the recursive form only (MTP input fusion, Sec. 3.1): the two
+    pre-fusion norm gains (1 + N(0, gain_std^2)), the fusion matrix w_fc [d][2d]
+    (N(0, weight_std^2)) and the base model's last hidden state of every
+    sequence, hidden_last [B][d] ~ N(0, 1), all in the storage dtype."""
+    dt = TORCH_DTYPE[w.dtype]
+    d = w.hidden
+    return {
+        "fc_norm_hidden": _normal((d,), 1.0, w.gain_std, dt, device, _gen(w, "fc_norm_hidden", device)),
+        "fc_norm_embed": _normal((d,), 1.0, w.gain_std, dt, device, _gen(w, "fc_norm_embed", device)),
+        "w_fc": _normal((d, 2 * d), 0.0, w.weight_std, dt, device, _gen(w, "w_fc", device)),
+        "hidden_last": _normal((w.batch, d), 0.0, 1.0, dt, device, _gen(w, "hidden_last", device)),
+    }
 
 
 @dataclass

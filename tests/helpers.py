@@ -56,3 +56,25 @@ def check_logits(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -
         assert np.array_equal(np.argmax(got, 1)[decisive], np.argmax(ref, 1)[decisive]), \
             f"{what}: argmax differs on a decisive row"
     return err
+
+
+def oracle_weights_recursive(params: dict, fusion: dict) -> dict:
+    W = oracle_weights(params)
+    f = {k: v.detach().double().cpu().numpy() for k, v in fusion.items() if k != "hidden_last"}
+    W.update({"fc_norm_h": f["fc_norm_hidden"], "fc_norm_e": f["fc_norm_embed"], "w_fc": f["w_fc"]})
+    return W
+
+
+def oracle_outputs_recursive(w, kv: inputs.KVCache, params: dict, fusion: dict, batch_idx, W=None):
+    """Recursive SP-k oracle results for the sequences in batch_idx, from the exact
+    stored values (fusion: inputs.fusion_params, any device)."""
+    W = W if W is not None else oracle_weights_recursive(params, fusion)
+    soft = params["soft_prompt"].detach().double().cpu().numpy()
+    h_last = fusion["hidden_last"].detach().double().cpu().numpy()
+    shape = head_shape(w)
+    outs = []
+    for b in batch_idx:
+        k, v = kv.logical_kv(b)
+        outs.append(oracle.probe_sequence_recursive(k.double().cpu().numpy(), v.double().cpu().numpy(),
+                                                    soft, h_last[b], W, shape))
+    return outs

@@ -49,14 +49,14 @@ def test_status_strings():
 
 
 def test_struct_layouts_match_the_c_compiler(tmp_path):
-    """ctypes mirrors of the three ABI structs have the sizes and field offsets
+    """ctypes mirrors of the four ABI structs have the sizes and field offsets
     gcc gives the header's declarations."""
     import shutil
     import subprocess
     if shutil.which("gcc") is None:
         pytest.skip("gcc not available")
     structs = {"sp_probe_config": binding.sp_probe_config, "sp_kv_cache": binding.sp_kv_cache,
-               "sp_probe_weights": binding.sp_probe_weights}
+               "sp_probe_weights": binding.sp_probe_weights, "sp_probe_fusion": binding.sp_probe_fusion}
     lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', "int main(void) {"]
     for name, cls in structs.items():
         lines.append(f'  printf("{name} %zu\\n", sizeof({name}));')
@@ -92,7 +92,8 @@ def test_invalid_configs_are_rejected_without_a_device():
     w = configs.SMALL_BF16
     bad = [dict(head_dim=96), dict(n_kv_heads=3), dict(k=0), dict(k=65), dict(n_classes=0),
            dict(hidden=500), dict(intermediate=100), dict(split_len=300), dict(split_len=128),
-           dict(max_batch=0), dict(dtype=7), dict(flags=8)]
+           dict(max_batch=0), dict(dtype=7), dict(flags=8),
+           dict(max_batch=1 << 20)]  # projection operands past 32-bit byte offsets
     for kw in bad:
         cfg = binding.make_config(w)
         for k, v in kw.items():
@@ -108,6 +109,8 @@ def test_null_arguments():
     lib = binding.load()
     assert lib.sp_probe_init(None, None) == -1
     assert lib.sp_probe_forward(None, None, None, None, None, None, None, None) == -1
+    assert lib.sp_probe_forward_recursive(None, None, None, None, None, None, None, None, None, None) == -1
+    assert lib.sp_probe_plan_recursive(None, 1, None, None, None, None) == -1
     assert lib.sp_probe_destroy(None) == 0
     assert lib.sp_probe_tap_bytes(None, 0, 1) == 0
     assert lib.sp_probe_check_device_error(None, None) == -1
