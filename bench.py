@@ -8,8 +8,8 @@ with the MTP input fusion: k single-row passes of the head, each reading the
 whole cache once) on the recursive workload.
 
 Prints one JSON line:
-  value      classifications/s = batch / (wall time per step), timed over K steps
-             bracketed by device synchronisation;
+  value      classifications/s = batch x tasks / (wall time per step), timed over
+             K steps bracketed by device synchronisation (one task unless --tasks);
   roofline   the split-attention kernel (the dominant one on the long-context
              workload): algorithmic KV bytes per launch / its mean duration,
              from HIP events recorded on the launch stream around it in the timed
@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--mode", choices=("one-pass", "recursive"), default="one-pass")
     ap.add_argument("--workload", default=None)
+    ap.add_argument("--tasks", type=int, default=1,
+                    help="one-pass mode: monitoring tasks sharing the cache in one call")
+    ap.add_argument("--last-row-only", action="store_true",
+                    help="one-pass mode: run only the rows the LAST read-out uses past the attention")
     ap.add_argument("--split-len", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -133,13 +137,18 @@ def main():
     kv = inputs.kv_cache(w, lens, dev)
     params = inputs.params(w, dev)
     fusion = inputs.fusion_params(w, dev) if recursive else None
-    logits = torch.empty((w.batch, w.n_classes), dtype=torch.float32, device=dev)
-    probe = binding.Probe(w, split_len=args.split_len, flags=binding.SP_FLAG_PROFILE)
+    T = 1 if recursive else args.tasks
+    tasks = inputs.task_params(w, T, dev) if T > 1 else None
+    logits = torch.empty((w.batch, T, w.n_classes), dtype=torch.float32, device=dev)
+    flags = binding.SP_FLAG_PROFILE | (binding.SP_FLAG_LAST_ROW_ONLY if args.last_row_only else 0)
+    probe = binding.Probe(w, split_len=args.split_len, flags=flags, max_tasks=T)
     torch.cuda.synchronize()
 
     def step():
         if recursive:
             probe.forward_recursive(kv, params, fusion, logits)
+        elif tasks is not None:
+            probe.forward_multi(kv, params, tasks["soft_prompts"], tasks["w_cls"], tasks["b_cls"], logits)
         else:
             probe.forward(kv, params, logits)
 
@@ -166,14 +175,16 @@ def main():
     launches = w.k if recursive else 1   # attention launches per step
     attn_ms = stages["attention"] / (n_fwd * launches)
     achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
-    traffic = traffic_per_launch(w.name)
+    # counters are taken per launch shape: the workload, its task count and row pruning
+    variant = w.name + (f"_tasks{T}" if T > 1 else "") + ("_last_row_only" if args.last_row_only else "")
+    traffic = traffic_per_launch(variant)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": "attn_split_bf16" if w.dtype == "bf16" else "attn_split_f32",
                 "algorithmic_bytes_per_launch": kv_bytes, "mean_launch_ms": round(attn_ms, 4)}
     plan = probe.plan_recursive(w.batch) if recursive else probe.plan(w.batch)
     out = {
-        "metric": METRIC if not recursive else "recursive SP-k classifications/sec at 1 MI355X", "value": round(w.batch / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
+        "metric": (METRIC if not recursive else "recursive SP-k classifications/sec at 1 MI355X"), "value": round(w.batch * T / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic (seeded; random-init head weights; paged KV ~N(0,1))",
@@ -182,7 +193,8 @@ def main():
                    "head_dim": w.head_dim, "intermediate": w.intermediate, "n_classes": w.n_classes,
                    "kv_layout": w.layout, "block_size": kv.block_size, "kv_bytes": kv_bytes,
                    "split_len": plan["split_len"], "parallelism": "single GPU",
-                   "mode": args.mode, "attention_launches_per_step": launches},
+                   "mode": args.mode, "attention_launches_per_step": launches, "tasks": T,
+                   "last_row_only": bool(args.last_row_only)},
         "roofline": roofline,
         "attention_gbps": round(achieved, 1),
         "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},

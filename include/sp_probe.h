@@ -68,7 +68,13 @@ typedef enum sp_pool {
 enum {
   SP_FLAG_DEBUG = 1,    /* validate device-resident seq_lens and block ids on every forward;
                            kernels then skip work after a failed check */
-  SP_FLAG_PROFILE = 2   /* record HIP events around every stage of each forward */
+  SP_FLAG_PROFILE = 2,  /* record HIP events around every stage of each forward */
+  SP_FLAG_LAST_ROW_ONLY = 4  /* one-pass forwards under SP_POOL_LAST compute only what the
+                                read-out uses: every soft row's key and value, but the queries,
+                                attention output, o-projection, MLP and final norm of the last
+                                soft row of each task alone (the other rows reach the logits only
+                                through their keys and values).  Same logits up to rounding order;
+                                requires SP_POOL_LAST */
 };
 
 /* Shape of the frozen head and limits of a handle. */
@@ -90,6 +96,8 @@ typedef struct sp_probe_config {
                             otherwise larger values are clamped to it) */
   int32_t split_len;     /* tokens per attention split, a power of two >= 256; 0 = automatic */
   int32_t flags;         /* SP_FLAG_* */
+  int32_t max_tasks;     /* largest task count of sp_probe_forward_multi, 1..64 (0 = 1);
+                            max_tasks * k <= 1024 */
 } sp_probe_config;
 
 /* The head's resident KV cache (Sec. 3.3 Eq. 2-3: K_{1:n}, V_{1:n}), read-only.
@@ -189,6 +197,22 @@ int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv_cache, const
                                const void* hidden_last, const sp_probe_fusion* fusion,
                                const sp_probe_weights* weights, float* logits, void* stream);
 
+/* Several monitoring tasks over one cache in one call (Sec. 3.3: one pass over
+ * the cached K/V serves every task).  Task t has its own k soft-prompt rows and
+ * its own classifier; the frozen head is shared.  Each task's soft rows sit at
+ * positions N_b .. N_b+k-1 and attend to the cache and causally to the soft rows
+ * of their own task only, so every task's logits equal those of sp_probe_forward
+ * with that task's soft prompt and classifier.
+ *   n_tasks      1 .. max_tasks of the handle
+ *   soft_prompts device [n_tasks][k][d]
+ *   weights      the frozen head as for sp_probe_forward; w_cls is [n_tasks][C][d]
+ *                and b_cls (nullable) [n_tasks][C]
+ *   logits       device fp32 [B][n_tasks][C]
+ * Everything else as sp_probe_forward; sp_probe_forward is the n_tasks = 1 case. */
+int sp_probe_forward_multi(sp_probe_t* h, const sp_kv_cache* kv_cache, const int32_t* seq_lens,
+                           const int32_t* block_table, int32_t n_tasks, const void* soft_prompts,
+                           const sp_probe_weights* weights, float* logits, void* stream);
+
 /* Free the workspace and the handle (waits for the device). NULL is accepted. */
 int sp_probe_destroy(sp_probe_t* h);
 
@@ -196,13 +220,16 @@ int sp_probe_destroy(sp_probe_t* h);
 const char* sp_probe_status_string(int status);
 
 /* Intermediate values of the last forward, for tests.  Row b*k + j is soft row
- * j (one-pass) or step j (recursive) of sequence b.  tap selects:
- *   SP_TAP_QKV   fp32 [k][(n_q + 2 n_kv) hd]   projections of the normed soft rows
- *                                              (one-pass forward only)
- *   SP_TAP_ATTN  [B k][n_q hd]                 attention output (fp16 for SP_BF16,
+ * j (one-pass) or step j (recursive) of sequence b; with T tasks, row
+ * (b*T + t)*k + j is soft row j of task t; with SP_FLAG_LAST_ROW_ONLY the
+ * one-pass forwards fill row b*T + t with task t's last soft row.  Sizes are
+ * for max_tasks tasks.  tap selects:
+ *   SP_TAP_QKV   fp32 [T k][(n_q + 2 n_kv) hd]  projections of the normed soft rows
+ *                                              (one-pass forwards only)
+ *   SP_TAP_ATTN  [B T k][n_q hd]               attention output (fp16 for SP_BF16,
  *                                              fp32 for SP_F32)
- *   SP_TAP_A     fp32 [B k][d]                 residual after the o-projection
- *   SP_TAP_Y     fp32 [B k][d]                 residual after the MLP
+ *   SP_TAP_A     fp32 [B T k][d]               residual after the o-projection
+ *   SP_TAP_Y     fp32 [B T k][d]               residual after the MLP
  *   SP_TAP_X     fp32 [B k][d]                 fused input rows x_t (recursive forward only)
  * sp_probe_tap_bytes returns the size for a batch; sp_probe_copy_tap enqueues a
  * device-to-device copy of it into dst (device, dst_bytes >= that size). */
@@ -227,7 +254,8 @@ int sp_probe_check_device_error(sp_probe_t* h, void* stream);
 int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stages, int32_t* n_forwards);
 
 /* Split plan of a handle: tokens per attention split and the launch grid of
- * the split-attention kernel for a batch (for measurement and tests). */
+ * the split-attention kernel of a one-task one-pass forward (honouring
+ * SP_FLAG_LAST_ROW_ONLY) for a batch (for measurement and tests). */
 int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len, int32_t* max_splits,
                   int32_t* rows_per_kv_head, int32_t* query_groups);
 /* The same for the attention of a recursive step (G query rows per KV head). */

@@ -271,3 +271,21 @@ def probe_batch_recursive(kv_list, soft_prompt, h_last, weights: dict, shape: He
             for b, (kc, vc) in enumerate(kv_list)]
     logits = np.stack([o["logits"] for o in outs]) if outs else np.zeros((0, f64(weights["w_cls"]).shape[0]))
     return (logits, outs) if taps else logits
+
+
+# ---------------------------------------------------------------- several tasks on one cache
+#
+# Sec. 3.3 (cost paragraph): classifiers with different soft prompts and heads
+# can share the same KV cache, so several monitoring tasks run at once.  Each
+# task is an independent probe: its soft rows see the cache and their own
+# task's soft rows only, and it has its own classifier.  The definition is
+# therefore the single-task probe once per task.
+
+def probe_batch_tasks(kv_list, soft_prompts, w_cls, b_cls, weights: dict, shape: HeadShape):
+    """Logits [B, T, C]: task t uses soft_prompts[t] ([k, d]), w_cls[t] ([C, d]) and
+    b_cls[t] (or no bias when b_cls is None) with the shared frozen head."""
+    per_task = []
+    for t in range(len(soft_prompts)):
+        W = dict(weights, w_cls=w_cls[t], b_cls=None if b_cls is None else b_cls[t])
+        per_task.append(probe_batch(kv_list, soft_prompts[t], W, shape))
+    return np.stack(per_task, axis=1)

@@ -19,14 +19,14 @@ STATUS = {0: "SP_OK", -1: "SP_ERR_INVALID_ARG", -2: "SP_ERR_UNSUPPORTED", -3: "S
           -7: "SP_ERR_DEVICE_DATA"}
 SP_F32, SP_BF16 = 0, 1
 SP_POOL_LAST, SP_POOL_MEAN = 0, 1
-SP_FLAG_DEBUG, SP_FLAG_PROFILE = 1, 2
+SP_FLAG_DEBUG, SP_FLAG_PROFILE, SP_FLAG_LAST_ROW_ONLY = 1, 2, 4
 SP_TAP_QKV, SP_TAP_ATTN, SP_TAP_A, SP_TAP_Y, SP_TAP_X = 0, 1, 2, 3, 4
 SP_N_STAGES = 8
 STAGES = ("soft_prep", "attention", "merge", "o_proj", "post_norm", "gate_up", "down", "classifier")
 
 # Every function the header declares, with its C signature.
 EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward",
-           "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
+           "sp_probe_forward_multi", "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
            "sp_probe_tap_bytes", "sp_probe_copy_tap", "sp_probe_check_device_error",
            "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive")
 
@@ -38,7 +38,8 @@ class sp_probe_config(ctypes.Structure):
                 ("n_classes", ctypes.c_int32), ("dtype", ctypes.c_int32), ("pool", ctypes.c_int32),
                 ("rms_eps", ctypes.c_float), ("rope_base", ctypes.c_double),
                 ("max_batch", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
-                ("split_len", ctypes.c_int32), ("flags", ctypes.c_int32)]
+                ("split_len", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("max_tasks", ctypes.c_int32)]
 
 
 class sp_kv_cache(ctypes.Structure):
@@ -81,6 +82,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_init.restype = ctypes.c_int
     lib.sp_probe_forward.argtypes = [vp, P(sp_kv_cache), vp, vp, vp, P(sp_probe_weights), vp, vp]
     lib.sp_probe_forward.restype = ctypes.c_int
+    lib.sp_probe_forward_multi.argtypes = [vp, P(sp_kv_cache), vp, vp, ctypes.c_int32, vp,
+                                           P(sp_probe_weights), vp, vp]
+    lib.sp_probe_forward_multi.restype = ctypes.c_int
     lib.sp_probe_forward_recursive.argtypes = [vp, P(sp_kv_cache), vp, vp, vp, vp, P(sp_probe_fusion),
                                                P(sp_probe_weights), vp, vp]
     lib.sp_probe_forward_recursive.restype = ctypes.c_int
@@ -137,6 +141,12 @@ def sp_probe_forward(h, kv: sp_kv_cache, seq_lens, block_table, soft_prompt,
                                    ctypes.byref(weights), logits, stream)
 
 
+def sp_probe_forward_multi(h, kv: sp_kv_cache, seq_lens, block_table, n_tasks: int, soft_prompts,
+                           weights: sp_probe_weights, logits, stream) -> int:
+    return load().sp_probe_forward_multi(h, ctypes.byref(kv), seq_lens, block_table, n_tasks,
+                                         soft_prompts, ctypes.byref(weights), logits, stream)
+
+
 def sp_probe_forward_recursive(h, kv: sp_kv_cache, seq_lens, block_table, soft_prompt, hidden_last,
                                fusion: sp_probe_fusion, weights: sp_probe_weights, logits, stream) -> int:
     return load().sp_probe_forward_recursive(h, ctypes.byref(kv), seq_lens, block_table, soft_prompt,
@@ -155,7 +165,7 @@ def sp_probe_status_string(status: int) -> str:
 # ---------------------------------------------------------------- torch-facing helpers
 
 def make_config(w, max_batch: Optional[int] = None, max_seq_len: Optional[int] = None,
-                split_len: int = 0, flags: int = 0) -> sp_probe_config:
+                split_len: int = 0, flags: int = 0, max_tasks: int = 1) -> sp_probe_config:
     """sp_probe_config for a paper_2608_28099_amd.configs.Workload."""
     return sp_probe_config(
         hidden=w.hidden, n_q_heads=w.n_q_heads, n_kv_heads=w.n_kv_heads, head_dim=w.head_dim,
@@ -165,7 +175,7 @@ def make_config(w, max_batch: Optional[int] = None, max_seq_len: Optional[int] =
         rms_eps=w.rms_eps, rope_base=w.rope_base,
         max_batch=max_batch if max_batch is not None else w.batch,
         max_seq_len=max_seq_len if max_seq_len is not None else w.max_seq_len(),
-        split_len=split_len, flags=flags)
+        split_len=split_len, flags=flags, max_tasks=max_tasks)
 
 
 def make_kv(kv, batch: Optional[int] = None) -> sp_kv_cache:
@@ -193,9 +203,9 @@ def make_fusion(fusion: dict) -> sp_probe_fusion:
 class Probe:
     """One library handle (workspace) for a workload shape."""
 
-    def __init__(self, w, max_batch=None, max_seq_len=None, split_len=0, flags=0):
+    def __init__(self, w, max_batch=None, max_seq_len=None, split_len=0, flags=0, max_tasks=1):
         self.w = w
-        self.cfg = make_config(w, max_batch, max_seq_len, split_len, flags)
+        self.cfg = make_config(w, max_batch, max_seq_len, split_len, flags, max_tasks)
         self.h = sp_probe_init(self.cfg)
         self.lib = load()
 
@@ -222,6 +232,24 @@ class Probe:
         st = sp_probe_forward(self.h, self._kv, kv.seq_lens.data_ptr(), _ptr(kv.block_table),
                               params["soft_prompt"].data_ptr(), self._wt, logits.data_ptr(), stream)
         _check(st, "sp_probe_forward")
+        return logits
+
+    def forward_multi(self, kv, params: dict, soft_prompts, w_cls, b_cls=None, logits=None,
+                      stream=None, batch=None):
+        """T tasks in one call: soft_prompts [T][k][d], w_cls [T][C][d], b_cls [T][C] or
+        None (the rest of params is the shared head); returns logits [B][T][C]."""
+        import torch
+        B = kv.seq_lens.shape[0] if batch is None else batch
+        T = soft_prompts.shape[0]
+        if logits is None:
+            logits = torch.empty((B, T, self.w.n_classes), dtype=torch.float32, device=kv.pool.device)
+        if stream is None:
+            stream = torch.cuda.current_stream(kv.pool.device).cuda_stream
+        self._kv = make_kv(kv, B)
+        self._wt = make_weights(dict(params, w_cls=w_cls, b_cls=b_cls))
+        st = sp_probe_forward_multi(self.h, self._kv, kv.seq_lens.data_ptr(), _ptr(kv.block_table), T,
+                                    soft_prompts.data_ptr(), self._wt, logits.data_ptr(), stream)
+        _check(st, "sp_probe_forward_multi")
         return logits
 
     def forward_recursive(self, kv, params: dict, fusion: dict, logits=None, stream=None, batch=None):

@@ -533,7 +533,9 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
   const int64_t base = ((int64_t)b * p.n_kv + g) * p.max_splits * p.r_alloc + r;
-  const int j = p.step + r / p.group, h = g * p.group + r % p.group;
+  const int qi = r / p.group, h = g * p.group + r % p.group;
+  const int j_lo = (qi / p.q_per_task) * p.k_task;                    // the task's first soft key
+  const int j = j_lo + p.q_first + qi % p.q_per_task + p.step;        // this row's soft row
   const int i0 = lane * DPL;
 
   const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + r) * p.hd + i0;
@@ -541,37 +543,39 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   const int64_t vo = ((p.per_seq ? (int64_t)b * p.n_kv : 0) + g) * p.ks * p.hd + i0;  // [ks][hd]
   float qv[DPL];
   soft_load<TI, DPL>(p.q, p.q_lo, qo, qv);
-  // soft scores in log2 units (q carries log2(e)/sqrt(hd)); lane jj keeps key jj's.
-  // Slots past j (up to the tile width ks, a multiple of 32) are read but unused.
+  // soft scores in log2 units (q carries log2(e)/sqrt(hd)); lane l keeps key j_lo + l's
+  // (a task has at most 64 soft rows).  Batch slots past j re-read key j, unused.
   float my = -INFINITY;
-  for (int j0 = 0; j0 <= j; j0 += C) {
+  for (int j0 = j_lo; j0 <= j; j0 += C) {
     float kv[C][DPL];
 #pragma unroll
-    for (int c = 0; c < C; ++c) soft_load<TI, DPL>(p.k_soft, p.k_soft_lo, ko + (int64_t)(j0 + c) * p.hd, kv[c]);
+    for (int c = 0; c < C; ++c)
+      soft_load<TI, DPL>(p.k_soft, p.k_soft_lo, ko + (int64_t)min(j0 + c, j) * p.hd, kv[c]);
 #pragma unroll
     for (int c = 0; c < C; ++c) {
       float part = 0.f;
 #pragma unroll
       for (int d = 0; d < DPL; ++d) part += qv[d] * kv[c][d];
       for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o);
-      if (lane == j0 + c && j0 + c <= j) my = part;
+      if (lane == j0 + c - j_lo && j0 + c <= j) my = part;
     }
   }
-  float M = my;  // key 0 is always visible: finite
+  float M = my;  // key j_lo is always visible: finite
   for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-  const float pj = lane <= j ? fast_exp2(my - M) : 0.f;
+  const float pj = lane <= j - j_lo ? fast_exp2(my - M) : 0.f;
   float L = pj;
   for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
   float acc[DPL];
 #pragma unroll
   for (int d = 0; d < DPL; ++d) acc[d] = 0.f;
-  for (int j0 = 0; j0 <= j; j0 += C) {
+  for (int j0 = j_lo; j0 <= j; j0 += C) {
     float vv[C][DPL];
 #pragma unroll
-    for (int c = 0; c < C; ++c) soft_load<TI, DPL>(p.v_soft, p.v_soft_lo, vo + (int64_t)(j0 + c) * p.hd, vv[c]);
+    for (int c = 0; c < C; ++c)
+      soft_load<TI, DPL>(p.v_soft, p.v_soft_lo, vo + (int64_t)min(j0 + c, j) * p.hd, vv[c]);
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-      const float pk = __shfl(pj, j0 + c);
+      const float pk = __shfl(pj, j0 + c - j_lo);
       if (j0 + c <= j)  // slots past j may hold anything, NaN included
 #pragma unroll
         for (int d = 0; d < DPL; ++d) acc[d] += pk * vv[c][d];
@@ -608,7 +612,8 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
     M = mn;
   }
   const float inv = 1.0f / L;
-  TO* out = (TO*)p.out + ((int64_t)b * p.k + j) * ((int64_t)p.n_q * p.hd) + (int64_t)h * p.hd + i0;
+  TO* out = (TO*)p.out + ((int64_t)b * p.out_rows + p.out_off + qi) * ((int64_t)p.n_q * p.hd) +
+            (int64_t)h * p.hd + i0;
 #pragma unroll
   for (int d = 0; d < DPL; ++d) out[d] = from_f32<TO>(acc[d] * inv);
 }

@@ -156,7 +156,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
           const int n = n0 + wn * WN + 16 * j + li;
           float v = acc[i][j][r];
           if (EPI == kEpiResidRow)
-            v += (float)((const bf16*)p.r)[(int64_t)(m % p.r_mod) * p.N + n];
+            v += (float)((const bf16*)p.r)[(int64_t)(m % p.r_mod) * p.r_ld + n];
           else if (EPI == kEpiResidF32)
             v += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
           ((float*)p.c)[(int64_t)m * p.ldc + n] = v;
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   const float* w = row(n);
   float acc = 0.f;
   for (int k = 0; k < p.K; ++k) acc += a[k] * w[k];
-  if (EPI == kEpiResidRow) acc += ((const float*)p.r)[(int64_t)(m % p.r_mod) * p.N + n];
+  if (EPI == kEpiResidRow) acc += ((const float*)p.r)[(int64_t)(m % p.r_mod) * p.r_ld + n];
   if (EPI == kEpiResidF32) acc += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }

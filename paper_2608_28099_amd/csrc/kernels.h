@@ -17,6 +17,11 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
                                int64_t ld_x, const void* gain, const void* gain2, void* out,
                                int64_t ld_out, int rows, int d, float eps, hipStream_t s);
 
+// Soft rows j = 0..k-1 of a launch belong to tasks of k_task rows each (one-pass:
+// every task's soft prompt; recursive: k = k_task = 1).  Row j of its task
+// (jj = j % k_task) sits at position N_b + step + jj and fills soft key/value
+// slot step + j; only rows jj >= q_first carry queries, which go to query row
+// (j / k_task) * q_per_task + jj - q_first of the sequence.
 struct RopeParams {
   const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32 ([B][k][...] when per_seq)
   const int* seq_lens;     // device [B]
@@ -30,8 +35,9 @@ struct RopeParams {
   void* k_soft_lo;
   void* v_soft_lo;
   int n_q, n_kv, hd, k, group, r_alloc, ks, max_seq_len;
-  int step;                // rows j go to position N_b + step + j and soft slot step + j
+  int step;                // position and slot offset (recursive step)
   int per_seq;             // projections and values per sequence (recursive steps)
+  int k_task, q_first, q_per_task;
   double rope_base;
   float q_scale;           // log2(e) / sqrt(hd)
 };
@@ -72,9 +78,13 @@ struct MergeParams {
   const void* k_soft_lo;
   const void* v_soft;
   const void* v_soft_lo;
-  void* out;               // [B k][n_q hd] (activation dtype)
-  int n_kv, group, k, rows, r_alloc, hd, ks, max_splits, split_len, max_seq_len, n_q;
-  int step;                // row r is soft row step + r / group (sees soft keys 0..that row)
+  void* out;               // [B out_rows][n_q hd] (activation dtype)
+  int n_kv, group, rows, r_alloc, hd, ks, max_splits, split_len, max_seq_len, n_q;
+  // Row r holds query qi = r / group of its sequence: soft row
+  // j = (qi / q_per_task) * k_task + q_first + qi % q_per_task + step, which
+  // sees the soft keys of its own task up to itself, [(qi / q_per_task) * k_task, j];
+  // its output goes to row b * out_rows + out_off + qi.
+  int k_task, q_first, q_per_task, step, out_rows, out_off;
   int per_seq;             // v_soft is [B][n_kv][ks][hd] instead of [n_kv][ks][hd]
 };
 // dt: storage dtype of the config (the output is fp16 for bf16 storage)
@@ -83,7 +93,7 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
 // ---------------------------------------------------------------- GEMM
 enum Epilogue {
   kEpiStore = 0,      // C fp32 = acc
-  kEpiResidRow = 1,   // C fp32 = acc + R[m % r_mod][n]   (R in the storage dtype)
+  kEpiResidRow = 1,   // C fp32 = acc + R[(m % r_mod) * r_ld + n]   (R in the storage dtype)
   kEpiResidF32 = 2,   // C fp32 = acc + R[m * r_ld + n]   (R fp32; r_ld 0 = one row for all m)
   kEpiSwiglu = 3      // C (activation dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
 };
@@ -102,12 +112,12 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
 
 // ---------------------------------------------------------------- read-out
 struct ClsParams {
-  const float* y;          // [B k][d]
+  const float* y;          // [B][n_tasks][k][d]: k rows per task
   const void* final_norm;  // [d]
-  const void* w_cls;       // [C][d]
-  const float* b_cls;      // nullable
-  float* logits;           // [B][C]
-  int k, d, n_classes, pool_mean;
+  const void* w_cls;       // [n_tasks][C][d]
+  const float* b_cls;      // nullable, [n_tasks][C]
+  float* logits;           // [B][n_tasks][C]
+  int k, d, n_classes, pool_mean, n_tasks;
   float eps;
 };
 hipError_t launch_final_classifier(DType dt, const ClsParams& p, int batch, hipStream_t s);

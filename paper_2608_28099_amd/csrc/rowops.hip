@@ -89,12 +89,13 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, c
 
 // ---------------------------------------------------------------- RoPE + scatter
 // One workgroup per (soft row j, sequence b): the rotation of pair (i, i + hd/2)
-// at position N_b + t, t = step + j, by angle (N_b + t) * base^(-2i/hd) is
-// computed once, in fp64, into LDS, then applied to every query and key head of
-// the row, which goes to soft slot t.  The value heads are not rotated; in the
-// one-pass form (per_seq = 0) they are the same for every sequence and written
-// by b = 0, in the recursive form every sequence has its own row of
-// projections ([B][k] rows) and its own values.
+// at the row's position N_b + t (t = step + j % k_task) by angle
+// (N_b + t) * base^(-2i/hd) is computed once, in fp64, into LDS, then applied
+// to the row's key heads (soft slot step + j) and, for rows that carry queries,
+// its query heads.  The value heads are not rotated; in the one-pass form
+// (per_seq = 0) they are the same for every sequence and written by b = 0, in
+// the recursive form every sequence has its own row of projections ([B][k]
+// rows) and its own values.
 // SPLIT (T = bf16): each value x is stored as hi = bf16(x) and lo = bf16(x - hi).
 template <typename T, bool SPLIT>
 __device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
@@ -111,9 +112,10 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
   const int hd = p.hd, half = hd / 2;
   int n = p.seq_lens[b];
   n = n < 0 ? 0 : (n > p.max_seq_len ? p.max_seq_len : n);
+  const int jj = j % p.k_task;
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     const double theta = pow(p.rope_base, -2.0 * (double)i / (double)hd);
-    const double ang = (double)(n + p.step + j) * theta;
+    const double ang = (double)(n + p.step + jj) * theta;
     cs[i] = (float)cos(ang);
     sn[i] = (float)sin(ang);
   }
@@ -121,13 +123,14 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
   const int slot = p.step + j;
   const float* row = p.qkv + ((int64_t)(p.per_seq ? b * p.k : 0) + j) * (p.n_q + 2 * p.n_kv) * hd;
   const int nrot = (p.n_q + p.n_kv) * half;
-  for (int e = threadIdx.x; e < nrot; e += blockDim.x) {
+  const int qi = (j / p.k_task) * p.q_per_task + jj - p.q_first;
+  for (int e = jj >= p.q_first ? threadIdx.x : p.n_q * half + threadIdx.x; e < nrot; e += blockDim.x) {
     const int h = e / half, i = e % half;
     const float c = cs[i], s = sn[i];
     const float x0 = row[h * hd + i], x1 = row[h * hd + i + half];
     const float r0 = x0 * c - x1 * s, r1 = x1 * c + x0 * s;
     if (h < p.n_q) {
-      const int g = h / p.group, rr = j * p.group + h % p.group;
+      const int g = h / p.group, rr = qi * p.group + h % p.group;
       const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
       put<T, SPLIT>(p.q, p.q_lo, base + i, r0 * p.q_scale);
       put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
@@ -148,18 +151,19 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
 }
 
 // ---------------------------------------------------------------- read-out
-// One workgroup per (sequence b, class c):
-//   logits[b][c] = sum_j w_j * inv_j * sum_i W_cls[c][i] gamma_i y_j[i]  (+ bias[c]),
-// with inv_j = 1 / sqrt(mean_i y_j[i]^2 + eps) over the read-out rows j (the
-// last soft row, w = 1; or all k, w = 1/k): RMSNorm, pooling and the linear
+// One workgroup per (sequence b, task t, class c):
+//   logits[b][t][c] = sum_j w_j * inv_j * sum_i W_cls[t][c][i] gamma_i y_j[i]  (+ bias[t][c]),
+// with inv_j = 1 / sqrt(mean_i y_j[i]^2 + eps) over the read-out rows j of task
+// t (its last row, w = 1; or all k, w = 1/k): RMSNorm, pooling and the linear
 // classifier folded into one pass and one block reduction per row.
 template <typename T>
 __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
   __shared__ float red[4];
-  const int b = blockIdx.x, c = blockIdx.y, d = p.d;
+  const int b = blockIdx.x, tc = blockIdx.y, d = p.d;  // tc = task * C + class
+  const int task = tc / p.n_classes;
   const int j0 = p.pool_mean ? 0 : p.k - 1;
   const float w = p.pool_mean ? 1.0f / (float)p.k : 1.0f;
-  const T* wr = (const T*)p.w_cls + (int64_t)c * d;
+  const T* wr = (const T*)p.w_cls + (int64_t)tc * d;
   const T* gm = (const T*)p.final_norm;
   float wg[kRowChunks][4];  // W_cls[c][i] * gamma_i, reused for every row
 #pragma unroll
@@ -175,7 +179,7 @@ __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
   }
   float logit = 0.f;
   for (int j = j0; j < p.k; ++j) {
-    const float* yr = p.y + ((int64_t)b * p.k + j) * d;
+    const float* yr = p.y + (((int64_t)b * p.n_tasks + task) * p.k + j) * d;
     float ss = 0.f, dot = 0.f;
 #pragma unroll
     for (int q = 0; q < kRowChunks; ++q) {
@@ -194,7 +198,8 @@ __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
     dot = block_sum_256(dot, red);
     logit += w * dot / sqrtf(ss / (float)d + p.eps);
   }
-  if (threadIdx.x == 0) p.logits[(int64_t)b * p.n_classes + c] = logit + (p.b_cls ? p.b_cls[c] : 0.f);
+  if (threadIdx.x == 0)
+    p.logits[(int64_t)b * p.n_tasks * p.n_classes + tc] = logit + (p.b_cls ? p.b_cls[tc] : 0.f);
 }
 
 // ---------------------------------------------------------------- validation
@@ -253,7 +258,7 @@ hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStre
 
 hipError_t launch_final_classifier(DType dt, const ClsParams& p, int batch, hipStream_t s) {
   if (p.d % 4 || p.d > 1024 * kRowChunks) return hipErrorInvalidValue;
-  const dim3 grid(batch, p.n_classes);
+  const dim3 grid(batch, p.n_tasks * p.n_classes);
   if (dt == kBF16)
     hipLaunchKernelGGL(final_classifier<bf16>, grid, dim3(256), 0, s, p);
   else

@@ -37,7 +37,8 @@ struct AttnPlan {
 };
 
 struct Plan {
-  int group, rows, waves, n_qgroups, r_alloc, ks, nqkv, split_len, max_splits, esz;
+  int group, max_tasks, ks, ks_rec, nqkv, esz;
+  int q_rows;    // query rows per (sequence, KV head) the one-pass query buffer holds
   AttnPlan rec;  // recursive steps: one soft row (G query rows) per KV head
   // workspace offsets (bytes)
   size_t off_u, off_qkv, off_q, off_ksoft, off_vsoft, off_q_lo, off_ksoft_lo, off_vsoft_lo,
@@ -59,19 +60,23 @@ int check_config(const sp_probe_config* c) {
   if (c->n_q_heads % c->n_kv_heads) return SP_ERR_INVALID_ARG;
   if (!(c->rms_eps >= 0.0f) || !(c->rope_base > 0.0)) return SP_ERR_INVALID_ARG;
   if (c->split_len != 0 && (c->split_len < 256 || !is_pow2(c->split_len))) return SP_ERR_INVALID_ARG;
-  if (c->flags & ~(SP_FLAG_DEBUG | SP_FLAG_PROFILE)) return SP_ERR_INVALID_ARG;
+  if (c->flags & ~(SP_FLAG_DEBUG | SP_FLAG_PROFILE | SP_FLAG_LAST_ROW_ONLY)) return SP_ERR_INVALID_ARG;
+  if ((c->flags & SP_FLAG_LAST_ROW_ONLY) && c->pool != SP_POOL_LAST) return SP_ERR_INVALID_ARG;
+  if (c->max_tasks < 0 || c->max_tasks > 64) return SP_ERR_INVALID_ARG;
   if (c->head_dim != 64 && c->head_dim != 128) return SP_ERR_UNSUPPORTED;
   if (c->k > 64 || c->n_classes > 64) return SP_ERR_UNSUPPORTED;
+  const int64_t tasks = c->max_tasks > 0 ? c->max_tasks : 1;
+  if (tasks * c->k > 1024) return SP_ERR_UNSUPPORTED;
   const int mult = c->dtype == SP_BF16 ? 32 : 4;
   if (c->hidden % mult || c->intermediate % mult) return SP_ERR_UNSUPPORTED;
-  if (c->dtype == SP_F32 && c->k * (c->n_q_heads / c->n_kv_heads) > 64) return SP_ERR_UNSUPPORTED;
+  if (c->dtype == SP_F32 && tasks * c->k * (c->n_q_heads / c->n_kv_heads) > 64) return SP_ERR_UNSUPPORTED;
   if (c->hidden > 16384) return SP_ERR_UNSUPPORTED;
   if (c->dtype == SP_BF16) {
     // byte offsets inside one MFMA projection operand (activations [B k] rows,
     // or one weight matrix) are 32-bit
     const int64_t qw = (int64_t)c->n_q_heads * c->head_dim;
     const int64_t widest = std::max<int64_t>({c->hidden, qw, c->intermediate});
-    const int64_t rows = std::max<int64_t>({(int64_t)c->max_batch * c->k, qw, c->intermediate});
+    const int64_t rows = std::max<int64_t>({(int64_t)c->max_batch * tasks * c->k, qw, c->intermediate});
     if (rows * widest * 2 >= (int64_t(1) << 31)) return SP_ERR_UNSUPPORTED;
   }
   return SP_OK;
@@ -126,34 +131,49 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows) {
   return a;
 }
 
+int n_tasks_max(const sp_probe_config& c) { return c.max_tasks > 0 ? c.max_tasks : 1; }
+
+// Attention plan of a one-pass forward with n_tasks tasks: k G query rows per
+// task and KV head, or G under SP_FLAG_LAST_ROW_ONLY.
+AttnPlan one_pass_plan(const sp_probe_config& c, int n_tasks) {
+  const int group = c.n_q_heads / c.n_kv_heads;
+  const int per_task = (c.flags & SP_FLAG_LAST_ROW_ONLY) ? 1 : c.k;
+  return attn_plan(c, n_tasks * per_task * group);
+}
+
 Plan make_plan(const sp_probe_config& c) {
   Plan p{};
   p.esz = c.dtype == SP_BF16 ? 2 : 4;
   p.group = c.n_q_heads / c.n_kv_heads;
-  const AttnPlan one = attn_plan(c, c.k * p.group);
-  p.rows = one.rows; p.waves = one.waves; p.n_qgroups = one.n_qgroups; p.r_alloc = one.r_alloc;
-  p.split_len = one.split_len; p.max_splits = one.max_splits;
+  p.max_tasks = n_tasks_max(c);
   p.rec = attn_plan(c, p.group);
-  p.ks = ((c.k + 31) / 32) * 32;
+  const int S = p.max_tasks * c.k;       // soft rows of the largest call
+  p.ks = ((S + 31) / 32) * 32;
+  p.ks_rec = ((c.k + 31) / 32) * 32;
   p.nqkv = (c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  // split partials: the largest of every plan the handle can run
+  size_t part_rows = (size_t)p.rec.max_splits * p.rec.r_alloc;
+  p.q_rows = 0;
+  for (int t = 1; t <= p.max_tasks; ++t) {
+    const AttnPlan a = one_pass_plan(c, t);
+    part_rows = std::max(part_rows, (size_t)a.max_splits * a.r_alloc);
+    p.q_rows = std::max(p.q_rows, a.r_alloc);
+  }
 
-  const size_t B = (size_t)c.max_batch, M = B * c.k, d = c.hidden, hd = c.head_dim;
+  const size_t B = (size_t)c.max_batch, M = B * S, d = c.hidden, hd = c.head_dim;
   const size_t kv = (size_t)c.n_kv_heads, e = p.esz;
   size_t o = 0;
   auto take = [&](size_t bytes) { const size_t at = o; o = align256(o + bytes); return at; };
-  p.off_u = take((size_t)c.k * d * e);
-  p.off_qkv = take((size_t)c.k * p.nqkv * 4);
-  p.off_q = take(B * kv * p.r_alloc * hd * e);
+  p.off_u = take((size_t)S * d * e);
+  p.off_qkv = take((size_t)S * p.nqkv * 4);
+  p.off_q = take(B * kv * p.q_rows * hd * e);
   p.off_ksoft = take(B * kv * p.ks * hd * e);
   p.off_vsoft = take(kv * hd * p.ks * e);
   // remainders of the split bf16 queries and soft keys/values (bf16 storage only)
   const size_t lo = c.dtype == SP_BF16 ? 1 : 0;
-  p.off_q_lo = take(lo * B * kv * p.r_alloc * hd * e);
+  p.off_q_lo = take(lo * B * kv * p.q_rows * hd * e);
   p.off_ksoft_lo = take(lo * B * kv * p.ks * hd * e);
   p.off_vsoft_lo = take(lo * kv * hd * p.ks * e);
-  // split partials: shared by the one-pass and the recursive forwards
-  const size_t part_rows = std::max((size_t)p.max_splits * p.r_alloc,
-                                    (size_t)p.rec.max_splits * p.rec.r_alloc);
   p.off_opart = take(B * kv * part_rows * hd * 4);
   p.off_ml = take(B * kv * part_rows * 8);
   p.off_attn = take(M * c.n_q_heads * hd * e);
@@ -162,18 +182,19 @@ Plan make_plan(const sp_probe_config& c) {
   p.off_s = take(M * (size_t)c.intermediate * e);
   p.off_y = take(M * d * 4);
   p.off_err = take(256);
+  const size_t Mr = B * c.k;
   p.off_rq = take(B * kv * p.rec.r_alloc * hd * e);
   p.off_rq_lo = take(lo * B * kv * p.rec.r_alloc * hd * e);
-  p.off_rks = take(B * kv * p.ks * hd * e);
-  p.off_rks_lo = take(lo * B * kv * p.ks * hd * e);
-  p.off_rvs = take(B * kv * p.ks * hd * e);
-  p.off_rvs_lo = take(lo * B * kv * p.ks * hd * e);
+  p.off_rks = take(B * kv * p.ks_rec * hd * e);
+  p.off_rks_lo = take(lo * B * kv * p.ks_rec * hd * e);
+  p.off_rvs = take(B * kv * p.ks_rec * hd * e);
+  p.off_rvs_lo = take(lo * B * kv * p.ks_rec * hd * e);
   p.off_rqkv = take(B * p.nqkv * 4);
   p.off_ru = take(B * d * e);
   p.off_rhn = take(B * d * e);
   p.off_ren = take((size_t)c.k * d * e);
   p.off_rce = take((size_t)c.k * d * 4);
-  p.off_rx = take(M * d * 4);
+  p.off_rx = take(Mr * d * 4);
   p.total = o;
   return p;
 }
@@ -389,10 +410,11 @@ SP_API int sp_probe_destroy(sp_probe_t* h) {
 SP_API int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len, int32_t* max_splits,
                          int32_t* rows_per_kv_head, int32_t* query_groups) {
   if (!h || batch < 0) return SP_ERR_INVALID_ARG;
-  if (split_len) *split_len = h->plan.split_len;
-  if (max_splits) *max_splits = h->plan.max_splits;
-  if (rows_per_kv_head) *rows_per_kv_head = h->plan.rows;
-  if (query_groups) *query_groups = h->plan.n_qgroups;
+  const AttnPlan a = one_pass_plan(h->cfg, 1);
+  if (split_len) *split_len = a.split_len;
+  if (max_splits) *max_splits = a.max_splits;
+  if (rows_per_kv_head) *rows_per_kv_head = a.rows;
+  if (query_groups) *query_groups = a.n_qgroups;
   return SP_OK;
 }
 
@@ -409,13 +431,19 @@ SP_API int sp_probe_plan_recursive(const sp_probe_t* h, int32_t batch, int32_t* 
 
 #define SP_TRY(expr) do { if ((expr) != hipSuccess) return SP_ERR_HIP; } while (0)
 
-SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
-                            const int32_t* block_table, const void* soft_prompt,
-                            const sp_probe_weights* wt, float* logits, void* stream) {
+namespace {
+
+// The one-pass forward for n_tasks tasks (Sec. 3.2-3.3; one task is the plain
+// probe): all tasks' soft rows share one pass over the cache.
+int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
+                     const int32_t* block_table, int n_tasks, const void* soft_prompt,
+                     const sp_probe_weights* wt, float* logits, void* stream) {
   // ---- host-side checks: nothing is enqueued unless all pass
   bool noop = false;
   const int chk = check_forward(h, kv, seq_lens, block_table, soft_prompt, wt, logits, &noop);
-  if (chk != SP_OK || noop) return chk;
+  if (chk != SP_OK) return chk;
+  if (n_tasks < 1 || n_tasks > h->plan.max_tasks) return SP_ERR_INVALID_ARG;
+  if (noop) return SP_OK;
   const sp_probe_config& c = h->cfg;
   const Plan& pl = h->plan;
   const int B = kv->batch;
@@ -423,7 +451,13 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   hipStream_t s = (hipStream_t)stream;
   const DType dt = c.dtype == SP_BF16 ? kBF16 : kF32;   // storage: weights, soft prompt, KV
   const DType at_dt = c.dtype == SP_BF16 ? kF16 : kF32;  // activations feeding the MFMAs
-  const int d = c.hidden, hd = c.head_dim, I = c.intermediate, M = B * c.k;
+  const int d = c.hidden, hd = c.head_dim, I = c.intermediate, K = c.k;
+  const bool last_only = c.flags & SP_FLAG_LAST_ROW_ONLY;
+  const int S = n_tasks * K;                 // soft rows (keys and values)
+  const int Kq = last_only ? 1 : K;          // rows per task past the attention
+  const int R = n_tasks * Kq;                // rows per sequence past the attention
+  const int M = B * R;
+  const AttnPlan ak = one_pass_plan(c, n_tasks);
   const bool debug = c.flags & SP_FLAG_DEBUG;
   int* err = at<int>(h, pl.off_err);
   const int* errp = debug ? err : nullptr;
@@ -439,10 +473,10 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 0: soft rows — RMSNorm, Q/K/V on the k distinct rows, RoPE per sequence
+  // stage 0: soft rows — RMSNorm, Q/K/V on the S distinct rows, RoPE per sequence
   SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, d, wt->in_norm, nullptr,
-                             at<void>(h, pl.off_u), d, c.k, d, c.rms_eps, s));
-  SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_u), at<void>(h, pl.off_qkv), c.k), s));
+                             at<void>(h, pl.off_u), d, S, d, c.rms_eps, s));
+  SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_u), at<void>(h, pl.off_qkv), S), s));
   {
     RopeParams r{};
     r.qkv = at<float>(h, pl.off_qkv);
@@ -454,9 +488,10 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     r.q_lo = at<void>(h, pl.off_q_lo);
     r.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
     r.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
-    r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = c.k; r.group = pl.group;
-    r.r_alloc = pl.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
+    r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = S; r.group = pl.group;
+    r.r_alloc = ak.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
     r.step = 0; r.per_seq = 0;
+    r.k_task = K; r.q_first = K - Kq; r.q_per_task = Kq;
     r.rope_base = c.rope_base;
     r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
     SP_TRY(launch_rope_scatter(dt, r, B, s));
@@ -464,17 +499,16 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   if (!mark()) return SP_ERR_HIP;
 
   // stage 1: split attention over the cached K/V
-  const AttnPlan one{pl.rows, pl.waves, pl.n_qgroups, pl.r_alloc, pl.split_len, pl.max_splits};
-  const AttnParams ap = attn_params(c, one, kv, seq_lens, block_table, errp, at<void>(h, pl.off_q),
+  const AttnParams ap = attn_params(c, ak, kv, seq_lens, block_table, errp, at<void>(h, pl.off_q),
                                     at<void>(h, pl.off_q_lo), at<float>(h, pl.off_opart),
                                     at<float2>(h, pl.off_ml));
   if (dt == kBF16)
-    SP_TRY(launch_attention_bf16(ap, hd, pl.waves, B, s));
+    SP_TRY(launch_attention_bf16(ap, hd, ak.waves, B, s));
   else
     SP_TRY(launch_attention_f32(ap, hd, B, s));
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 2: merge the splits and the soft keys into the attention output rows b*k + j
+  // stage 2: merge the splits and each task's soft keys into the attention output rows
   {
     MergeParams mp{};
     mp.o_part = ap.o_part; mp.ml_part = ap.ml_part; mp.seq_lens = seq_lens; mp.err = errp;
@@ -482,19 +516,22 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
     mp.k_soft = at<void>(h, pl.off_ksoft); mp.k_soft_lo = at<void>(h, pl.off_ksoft_lo);
     mp.v_soft = at<void>(h, pl.off_vsoft); mp.v_soft_lo = at<void>(h, pl.off_vsoft_lo);
     mp.out = at<void>(h, pl.off_attn);
-    mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.k = c.k; mp.rows = pl.rows;
-    mp.r_alloc = pl.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = pl.max_splits;
-    mp.split_len = pl.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
-    mp.step = 0; mp.per_seq = 0;
+    mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.rows = ak.rows;
+    mp.r_alloc = ak.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = ak.max_splits;
+    mp.split_len = ak.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
+    mp.k_task = K; mp.q_first = K - Kq; mp.q_per_task = Kq; mp.step = 0;
+    mp.out_rows = R; mp.out_off = 0; mp.per_seq = 0;
     SP_TRY(launch_merge(dt, mp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 3: a = x_j + W_o o
+  // stage 3: a = x + W_o o, x the row's soft-prompt vector
   {
     const int qw = c.n_q_heads * hd;
     GemmParams g = gemm_one(at<void>(h, pl.off_attn), qw, wt->w_o, qw, at<void>(h, pl.off_a), d, M, d, qw);
-    g.r = soft_prompt; g.r_mod = c.k;
+    g.r = (const char*)soft_prompt + (size_t)(K - Kq) * d * pl.esz;
+    g.r_mod = R;
+    g.r_ld = last_only ? K * d : d;
     SP_TRY(launch_gemm(dt, kEpiResidRow, g, s));
   }
   if (!mark()) return SP_ERR_HIP;
@@ -516,19 +553,34 @@ SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t*
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 7: final RMSNorm, read-out, logits = W_cls pooled (+ b)
+  // stage 7: final RMSNorm, read-out, logits = W_cls pooled (+ b), per task
   {
     ClsParams cp{};
     cp.y = at<float>(h, pl.off_y);
     cp.final_norm = wt->final_norm; cp.w_cls = wt->w_cls; cp.b_cls = wt->b_cls;
     cp.logits = logits;
-    cp.k = c.k; cp.d = d; cp.n_classes = c.n_classes; cp.pool_mean = c.pool == SP_POOL_MEAN;
+    cp.k = Kq; cp.n_tasks = n_tasks; cp.d = d; cp.n_classes = c.n_classes;
+    cp.pool_mean = c.pool == SP_POOL_MEAN;
     cp.eps = c.rms_eps;
     SP_TRY(launch_final_classifier(dt, cp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
   if (ev) prof_commit(h, marks);
   return SP_OK;
+}
+
+}  // namespace
+
+SP_API int sp_probe_forward(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
+                            const int32_t* block_table, const void* soft_prompt,
+                            const sp_probe_weights* wt, float* logits, void* stream) {
+  return forward_one_pass(h, kv, seq_lens, block_table, 1, soft_prompt, wt, logits, stream);
+}
+
+SP_API int sp_probe_forward_multi(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
+                                  const int32_t* block_table, int32_t n_tasks, const void* soft_prompts,
+                                  const sp_probe_weights* wt, float* logits, void* stream) {
+  return forward_one_pass(h, kv, seq_lens, block_table, n_tasks, soft_prompts, wt, logits, stream);
 }
 
 SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_lens,
@@ -609,8 +661,9 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       r.k_soft_lo = at<void>(h, pl.off_rks_lo);
       r.v_soft_lo = at<void>(h, pl.off_rvs_lo);
       r.n_q = c.n_q_heads; r.n_kv = c.n_kv_heads; r.hd = hd; r.k = 1; r.group = pl.group;
-      r.r_alloc = rp.r_alloc; r.ks = pl.ks; r.max_seq_len = c.max_seq_len;
+      r.r_alloc = rp.r_alloc; r.ks = pl.ks_rec; r.max_seq_len = c.max_seq_len;
       r.step = t; r.per_seq = 1;
+      r.k_task = 1; r.q_first = 0; r.q_per_task = 1;
       r.rope_base = c.rope_base;
       r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
       SP_TRY(launch_rope_scatter(dt, r, B, s));
@@ -635,10 +688,11 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       mp.k_soft = at<void>(h, pl.off_rks); mp.k_soft_lo = at<void>(h, pl.off_rks_lo);
       mp.v_soft = at<void>(h, pl.off_rvs); mp.v_soft_lo = at<void>(h, pl.off_rvs_lo);
       mp.out = o_all;
-      mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.k = K; mp.rows = rp.rows;
-      mp.r_alloc = rp.r_alloc; mp.hd = hd; mp.ks = pl.ks; mp.max_splits = rp.max_splits;
+      mp.n_kv = c.n_kv_heads; mp.group = pl.group; mp.rows = rp.rows;
+      mp.r_alloc = rp.r_alloc; mp.hd = hd; mp.ks = pl.ks_rec; mp.max_splits = rp.max_splits;
       mp.split_len = rp.split_len; mp.max_seq_len = c.max_seq_len; mp.n_q = c.n_q_heads;
-      mp.step = t; mp.per_seq = 1;
+      mp.k_task = 1; mp.q_first = 0; mp.q_per_task = 1; mp.step = t;
+      mp.out_rows = K; mp.out_off = t; mp.per_seq = 1;
       SP_TRY(launch_merge(dt, mp, B, s));
     }
     if (!mark()) return SP_ERR_HIP;
@@ -681,7 +735,8 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       cp.y = (const float*)y_all;
       cp.final_norm = wt->final_norm; cp.w_cls = wt->w_cls; cp.b_cls = wt->b_cls;
       cp.logits = logits;
-      cp.k = K; cp.d = d; cp.n_classes = c.n_classes; cp.pool_mean = c.pool == SP_POOL_MEAN;
+      cp.k = K; cp.n_tasks = 1; cp.d = d; cp.n_classes = c.n_classes;
+      cp.pool_mean = c.pool == SP_POOL_MEAN;
       cp.eps = c.rms_eps;
       SP_TRY(launch_final_classifier(dt, cp, B, s));
     }
@@ -696,13 +751,13 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
 SP_API size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch) {
   if (!h || batch < 0 || batch > h->cfg.max_batch) return 0;
   const sp_probe_config& c = h->cfg;
-  const size_t M = (size_t)batch * c.k, e = h->plan.esz;
+  const size_t S = (size_t)h->plan.max_tasks * c.k, M = (size_t)batch * S, e = h->plan.esz;
   switch (tap) {
-    case SP_TAP_QKV: return (size_t)c.k * h->plan.nqkv * 4;
+    case SP_TAP_QKV: return S * h->plan.nqkv * 4;
     case SP_TAP_ATTN: return M * c.n_q_heads * c.head_dim * e;
     case SP_TAP_A: return M * c.hidden * 4;
     case SP_TAP_Y: return M * c.hidden * 4;
-    case SP_TAP_X: return M * c.hidden * 4;
+    case SP_TAP_X: return (size_t)batch * c.k * c.hidden * 4;
   }
   return 0;
 }

@@ -107,6 +107,21 @@ def params(w: Workload, device="cpu") -> dict:
     return p
 
 
+def task_params(w: Workload, n_tasks: int, device="cpu") -> dict:
+    """Per-task inputs of a multi-task call: soft_prompts [T][k][d], w_cls [T][C][d]
+    and b_cls [T][C] (None without a bias).  Task 0 has the single-task values of
+    params(); task t > 0 draws its own from the same distributions."""
+    dt = TORCH_DTYPE[w.dtype]
+    d = w.hidden
+    soft = [_normal((w.k, d), 0.0, w.soft_std, dt, device, _gen(w, "soft", device, t)) for t in range(n_tasks)]
+    wc = [_normal((w.n_classes, d), 0.0, w.weight_std, dt, device, _gen(w, "w_cls", device, t))
+          for t in range(n_tasks)]
+    bc = ([_normal((w.n_classes,), 0.0, 1.0, torch.float32, device, _gen(w, "b_cls", device, t))
+           for t in range(n_tasks)] if w.cls_bias else None)
+    return {"soft_prompts": torch.stack(soft).contiguous(), "w_cls": torch.stack(wc).contiguous(),
+            "b_cls": torch.stack(bc).contiguous() if bc is not None else None}
+
+
 def fusion_params(w: Workload, device="cpu") -> dict:
     """Inputs of the recursive form only (MTP input fusion, Sec. 3.1): the two
     pre-fusion norm gains (1 + N(0, gain_std^2)), the fusion matrix w_fc [d][2d]

@@ -93,7 +93,9 @@ def test_invalid_configs_are_rejected_without_a_device():
     bad = [dict(head_dim=96), dict(n_kv_heads=3), dict(k=0), dict(k=65), dict(n_classes=0),
            dict(hidden=500), dict(intermediate=100), dict(split_len=300), dict(split_len=128),
            dict(max_batch=0), dict(dtype=7), dict(flags=8),
-           dict(max_batch=1 << 20)]  # projection operands past 32-bit byte offsets
+           dict(max_batch=1 << 20),  # projection operands past 32-bit byte offsets
+           dict(max_tasks=65), dict(max_tasks=-1), dict(max_tasks=64, k=17),
+           dict(flags=4, pool=1)]     # last-row-only needs LAST pooling
     for kw in bad:
         cfg = binding.make_config(w)
         for k, v in kw.items():
@@ -114,3 +116,11 @@ def test_null_arguments():
     assert lib.sp_probe_destroy(None) == 0
     assert lib.sp_probe_tap_bytes(None, 0, 1) == 0
     assert lib.sp_probe_check_device_error(None, None) == -1
+
+
+def test_workspace_grows_with_tasks():
+    w = configs.QWEN9B_BF16
+    one = binding.sp_probe_workspace_bytes(binding.make_config(w))
+    four = binding.sp_probe_workspace_bytes(binding.make_config(w, max_tasks=4))
+    pruned = binding.sp_probe_workspace_bytes(binding.make_config(w, max_tasks=4, flags=binding.SP_FLAG_LAST_ROW_ONLY))
+    assert four > 3 * one // 2 and 0 < pruned

@@ -321,3 +321,29 @@ def test_trainable_parameter_counts():
     the "about 18K" of Sec. 1."""
     assert 1 * 4096 + 4096 == 8192
     assert 5 * 3584 == 17920
+
+
+def test_tasks_are_independent_probes():
+    """Sec. 3.3: classifiers sharing one cache are independent: task t's logits are
+    the single-task probe's with its own soft prompt and head, whatever the other
+    tasks hold; a permutation of the tasks permutes the output."""
+    rng = np.random.default_rng(51)
+    d, n_q, n_kv, hd, inter, k, C, T = 16, 4, 2, 4, 20, 3, 2, 3
+    W = rand_weights(rng, d, n_q, n_kv, hd, inter, C)
+    kvs = [tuple(rng.standard_normal((2, n_kv, n, hd))) for n in (4, 0, 7)]
+    soft = rng.standard_normal((T, k, d))
+    wc = rng.standard_normal((T, C, d))
+    bc = rng.standard_normal((T, C))
+    hs = O.HeadShape(n_q, n_kv, hd)
+    out = O.probe_batch_tasks(kvs, soft, wc, bc, W, hs)
+    assert out.shape == (3, T, C)
+    for t in range(T):
+        single = O.probe_batch(kvs, soft[t], dict(W, w_cls=wc[t], b_cls=bc[t]), hs)
+        np.testing.assert_array_equal(out[:, t], single)
+    soft2 = soft.copy()
+    soft2[1] = -soft2[1]
+    out2 = O.probe_batch_tasks(kvs, soft2, wc, bc, W, hs)
+    np.testing.assert_array_equal(out2[:, 0], out[:, 0])
+    np.testing.assert_array_equal(out2[:, 2], out[:, 2])
+    perm = [2, 0, 1]
+    np.testing.assert_array_equal(O.probe_batch_tasks(kvs, soft[perm], wc[perm], bc[perm], W, hs), out[:, perm])
