@@ -128,7 +128,14 @@ typedef struct sp_kv_cache {
  * config's dtype except b_cls (fp32), 16-byte aligned, [out, in] row-major:
  *   in_norm[d], w_q[n_q*hd][d], w_k[n_kv*hd][d], w_v[n_kv*hd][d], w_o[d][n_q*hd],
  *   post_norm[d], w_gate[I][d], w_up[I][d], w_down[d][I], final_norm[d],
- *   w_cls[C][d], b_cls[C] (nullable: no bias). */
+ *   w_cls[C][d], b_cls[C] (nullable: no bias).
+ * Read-out through a vocabulary matrix (the frozen LM-head ablation, Sec. 6.7,
+ * Table 7): with cls_rows set (device int32, one row index per class, [T][C]
+ * for a multi-task call), class c reads row cls_rows[c] of w_cls, which is then
+ * a [cls_vocab][d] matrix such as the head's LM head; with C = 2 and the rows of
+ * the "yes" and "no" tokens, logits[b][0] - logits[b][1] is the paper's yes/no
+ * score.  cls_rows NULL: w_cls is the trained [C][d] head (cls_vocab ignored).
+ * Debug mode checks 0 <= cls_rows[i] < cls_vocab. */
 typedef struct sp_probe_weights {
   const void* in_norm;
   const void* w_q;
@@ -142,6 +149,8 @@ typedef struct sp_probe_weights {
   const void* final_norm;
   const void* w_cls;
   const float* b_cls;
+  const int32_t* cls_rows;     /* nullable, device */
+  int64_t cls_vocab;           /* rows of w_cls when cls_rows is set */
 } sp_probe_weights;
 
 typedef struct sp_probe sp_probe_t;  /* opaque handle, library-owned */
@@ -177,6 +186,12 @@ typedef struct sp_probe_fusion {
   const void* fc_norm_hidden;
   const void* fc_norm_embed;
   const void* w_fc;
+  /* Eagle3 input (Sec. 3.1, Eagle3 paragraph): NULL for the MTP head, whose first
+   * hidden state is the base model's last layer (hidden_last [B][d]); else a
+   * [d][3d] matrix, hidden_last is [B][3d] (three of the base model's hidden
+   * states, low / mid / high layer, concatenated) and the first step's hidden
+   * state is w_hidden_fuse . hidden_last[b]. */
+  const void* w_hidden_fuse;
 } sp_probe_fusion;
 
 /* Recursive SP-k, the form the paper evaluates (Sec. 3.2, with the fusion of
@@ -188,7 +203,7 @@ typedef struct sp_probe_fusion {
  * keys of steps 0..t.  The read-out is the config's pool over the steps' f_t
  * (SP_POOL_LAST: f_{k-1}, the output of the k-th step).  The cache is read once
  * per step.
- *   hidden_last  device [B][d] in the config's dtype
+ *   hidden_last  device [B][d] in the config's dtype ([B][3d] with w_hidden_fuse)
  *   fusion       host struct of device pointers
  * Every other argument, the checks and the error behaviour are those of
  * sp_probe_forward; the same handle serves both forwards. */

@@ -123,13 +123,33 @@ def cached_attention(q_rot, k_cache, v_cache, k_soft, v_soft):
     return o, probs
 
 
+def read_out(W: dict, pooled: np.ndarray) -> np.ndarray:
+    """Logits of the pooled final hidden state: the linear head W_cls (Sec. 3.2), or,
+    when W holds ``cls_rows``, the rows of a vocabulary matrix W_cls (the frozen
+    LM head of the classification-head ablation, Sec. 6.7: with the rows of the
+    yes and no tokens, logits[0] - logits[1] is the yes/no score)."""
+    w_cls = W["w_cls"]
+    if W.get("cls_rows") is not None:
+        w_cls = w_cls[np.asarray(W["cls_rows"], dtype=np.int64)]
+    logits = w_cls @ pooled
+    if W.get("b_cls") is not None:
+        logits = logits + W["b_cls"]
+    return logits
+
+
+def _weights64(weights: dict) -> dict:
+    """Weights as fp64 arrays; integer row indices stay integers."""
+    return {key: (None if val is None else (np.asarray(val, dtype=np.int64) if key == "cls_rows" else f64(val)))
+            for key, val in weights.items()}
+
+
 def probe_sequence(k_cache, v_cache, soft_prompt, weights: dict, shape: HeadShape) -> dict:
     """Logits and intermediate values for one sequence.
 
     k_cache, v_cache: [n_kv, N, hd]; soft_prompt: [k, d]; weights: dict with
     in_norm, w_q, w_k, w_v, w_o, post_norm, w_gate, w_up, w_down, final_norm,
     w_cls ([out, in] matrices) and optional b_cls."""
-    W = {key: (None if val is None else f64(val)) for key, val in weights.items()}
+    W = _weights64(weights)
     x = f64(soft_prompt)
     k, d = x.shape
     n = int(np.shape(k_cache)[1])
@@ -156,9 +176,7 @@ def probe_sequence(k_cache, v_cache, soft_prompt, weights: dict, shape: HeadShap
         pooled = np.mean(f, axis=0)
     else:
         raise ValueError(shape.pool)
-    logits = W["w_cls"] @ pooled
-    if W.get("b_cls") is not None:
-        logits = logits + W["b_cls"]
+    logits = read_out(W, pooled)
     return {"u": u, "q_rot": q_rot, "k_rot": k_rot, "v": v, "probs": probs, "o": o_flat,
             "a": a, "s": s, "y": y, "f": f, "pooled": pooled, "logits": logits}
 
@@ -233,14 +251,20 @@ def probe_sequence_recursive(k_cache, v_cache, soft_prompt, h_last, weights: dic
     """Recursive SP-k logits and per-step values for one sequence.
 
     k_cache, v_cache: [n_kv, N, hd]; soft_prompt: [k, d] (e_1..e_k); h_last: [d],
-    the base model's last hidden state; weights: the one-pass keys plus
-    fc_norm_h [d], fc_norm_e [d] and w_fc [d][2d].  Returned arrays stack the
+    the base model's last hidden state ([3d] with w_hidden_fuse); weights: the
+    one-pass keys plus fc_norm_h [d], fc_norm_e [d], w_fc [d][2d] and optionally
+    w_hidden_fuse [d][3d] (Eagle3 input).  Returned arrays stack the
     steps: x, a, y, f are [k, d], o is [k, n_q*hd]."""
-    W = {key: (None if val is None else f64(val)) for key, val in weights.items()}
+    W = _weights64(weights)
     e = f64(soft_prompt)
     k, d = e.shape
     n = int(np.shape(k_cache)[1])
     h = f64(h_last)
+    if W.get("w_hidden_fuse") is not None:
+        # Eagle3 input (Sec. 3.1, Eagle3 paragraph): h_last holds three hidden
+        # states of the base model (low, mid, high layer) concatenated, and the
+        # first hidden state is their projection (no norm before it)
+        h = W["w_hidden_fuse"] @ h
     soft_k, soft_v, steps = [], [], []
     for t in range(k):
         z = np.concatenate([rms_norm(h, W["fc_norm_h"], shape.rms_eps),
@@ -256,9 +280,7 @@ def probe_sequence_recursive(k_cache, v_cache, soft_prompt, h_last, weights: dic
         pooled = np.mean(f, axis=0)
     else:
         raise ValueError(shape.pool)
-    logits = W["w_cls"] @ pooled
-    if W.get("b_cls") is not None:
-        logits = logits + W["b_cls"]
+    logits = read_out(W, pooled)
     out = {name: np.stack([st[name] for st in steps]) for name in ("x", "o", "a", "y", "f")}
     out.update({"probs": [st["probs"] for st in steps], "pooled": pooled, "logits": logits})
     return out
@@ -281,11 +303,16 @@ def probe_batch_recursive(kv_list, soft_prompt, h_last, weights: dict, shape: He
 # task's soft rows only, and it has its own classifier.  The definition is
 # therefore the single-task probe once per task.
 
-def probe_batch_tasks(kv_list, soft_prompts, w_cls, b_cls, weights: dict, shape: HeadShape):
+def probe_batch_tasks(kv_list, soft_prompts, w_cls, b_cls, weights: dict, shape: HeadShape,
+                      cls_rows=None):
     """Logits [B, T, C]: task t uses soft_prompts[t] ([k, d]), w_cls[t] ([C, d]) and
-    b_cls[t] (or no bias when b_cls is None) with the shared frozen head."""
+    b_cls[t] (or no bias when b_cls is None) with the shared frozen head.  With
+    cls_rows ([T, C]) w_cls is one vocabulary matrix and task t reads its rows
+    cls_rows[t]."""
     per_task = []
     for t in range(len(soft_prompts)):
-        W = dict(weights, w_cls=w_cls[t], b_cls=None if b_cls is None else b_cls[t])
+        W = dict(weights, w_cls=w_cls[t] if cls_rows is None else w_cls,
+                 b_cls=None if b_cls is None else b_cls[t],
+                 cls_rows=None if cls_rows is None else cls_rows[t])
         per_task.append(probe_batch(kv_list, soft_prompts[t], W, shape))
     return np.stack(per_task, axis=1)

@@ -54,12 +54,12 @@ class sp_kv_cache(ctypes.Structure):
 class sp_probe_weights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("in_norm", "w_q", "w_k", "w_v", "w_o", "post_norm", "w_gate", "w_up", "w_down",
-                 "final_norm", "w_cls", "b_cls")]
+                 "final_norm", "w_cls", "b_cls", "cls_rows")] + [("cls_vocab", ctypes.c_int64)]
 
 
 
 class sp_probe_fusion(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("fc_norm_hidden", "fc_norm_embed", "w_fc")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("fc_norm_hidden", "fc_norm_embed", "w_fc", "w_hidden_fuse")]
 
 
 _lib = None
@@ -191,13 +191,19 @@ def make_kv(kv, batch: Optional[int] = None) -> sp_kv_cache:
 
 
 def make_weights(params: dict) -> sp_probe_weights:
-    return sp_probe_weights(**{n: _ptr(params.get(n)) for n in
-                               ("in_norm", "w_q", "w_k", "w_v", "w_o", "post_norm", "w_gate",
-                                "w_up", "w_down", "final_norm", "w_cls", "b_cls")})
+    """params: the head's tensors; optional cls_rows (device int32) selects rows of
+    w_cls, a vocabulary matrix of cls_vocab rows (default: its first dimension)."""
+    wt = sp_probe_weights(**{n: _ptr(params.get(n)) for n in
+                             ("in_norm", "w_q", "w_k", "w_v", "w_o", "post_norm", "w_gate",
+                              "w_up", "w_down", "final_norm", "w_cls", "b_cls", "cls_rows")})
+    if params.get("cls_rows") is not None:
+        wt.cls_vocab = params.get("cls_vocab", params["w_cls"].shape[0])
+    return wt
 
 
 def make_fusion(fusion: dict) -> sp_probe_fusion:
-    return sp_probe_fusion(**{n: _ptr(fusion.get(n)) for n in ("fc_norm_hidden", "fc_norm_embed", "w_fc")})
+    return sp_probe_fusion(**{n: _ptr(fusion.get(n)) for n in
+                              ("fc_norm_hidden", "fc_norm_embed", "w_fc", "w_hidden_fuse")})
 
 
 class Probe:
@@ -235,7 +241,7 @@ class Probe:
         return logits
 
     def forward_multi(self, kv, params: dict, soft_prompts, w_cls, b_cls=None, logits=None,
-                      stream=None, batch=None):
+                      stream=None, batch=None, cls_rows=None):
         """T tasks in one call: soft_prompts [T][k][d], w_cls [T][C][d], b_cls [T][C] or
         None (the rest of params is the shared head); returns logits [B][T][C]."""
         import torch
@@ -246,7 +252,7 @@ class Probe:
         if stream is None:
             stream = torch.cuda.current_stream(kv.pool.device).cuda_stream
         self._kv = make_kv(kv, B)
-        self._wt = make_weights(dict(params, w_cls=w_cls, b_cls=b_cls))
+        self._wt = make_weights(dict(params, w_cls=w_cls, b_cls=b_cls, cls_rows=cls_rows))
         st = sp_probe_forward_multi(self.h, self._kv, kv.seq_lens.data_ptr(), _ptr(kv.block_table), T,
                                     soft_prompts.data_ptr(), self._wt, logits.data_ptr(), stream)
         _check(st, "sp_probe_forward_multi")

@@ -159,6 +159,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
             v += (float)((const bf16*)p.r)[(int64_t)(m % p.r_mod) * p.r_ld + n];
           else if (EPI == kEpiResidF32)
             v += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
+          else if (EPI == kEpiRowScale)
+            v *= ((const float*)p.r)[m];
           ((float*)p.c)[(int64_t)m * p.ldc + n] = v;
         }
       }
@@ -195,6 +197,7 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   for (int k = 0; k < p.K; ++k) acc += a[k] * w[k];
   if (EPI == kEpiResidRow) acc += ((const float*)p.r)[(int64_t)(m % p.r_mod) * p.r_ld + n];
   if (EPI == kEpiResidF32) acc += ((const float*)p.r)[(int64_t)m * p.r_ld + n];
+  if (EPI == kEpiRowScale) acc *= ((const float*)p.r)[m];
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }
 
@@ -206,6 +209,7 @@ hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
     case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore>), grid, block, 0, s, p); break;
     case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow>), grid, block, 0, s, p); break;
     case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32>), grid, block, 0, s, p); break;
+    case kEpiRowScale: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiRowScale>), grid, block, 0, s, p); break;
     case kEpiSwiglu:
       if constexpr ((BN / WGN) % 32 == 0)
         hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu>), grid, block, 0, s, p);
@@ -241,6 +245,7 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
       case kEpiStore: hipLaunchKernelGGL(gemm_f32<kEpiStore>, grid, dim3(256), 0, s, p); break;
       case kEpiResidRow: hipLaunchKernelGGL(gemm_f32<kEpiResidRow>, grid, dim3(256), 0, s, p); break;
       case kEpiResidF32: hipLaunchKernelGGL(gemm_f32<kEpiResidF32>, grid, dim3(256), 0, s, p); break;
+      case kEpiRowScale: hipLaunchKernelGGL(gemm_f32<kEpiRowScale>, grid, dim3(256), 0, s, p); break;
       case kEpiSwiglu: hipLaunchKernelGGL(gemm_f32<kEpiSwiglu>, grid, dim3(256), 0, s, p); break;
     }
     return hipGetLastError();

@@ -44,6 +44,12 @@ struct RopeParams {
 // dt: output type: kF32, or kBF16 for the hi/lo bf16 split
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s);
 
+// fp16 copy of bf16 rows scaled by a power of two so that no value exceeds the
+// fp16 range: out[r][i] = x[r][i] * 2^-e_r, inv_scale[r] = 2^e_r, with e_r >= 0
+// the smallest exponent that brings max_i |x[r][i]| * 2^-e_r below 2^15.
+hipError_t launch_scale_rows_f16(const void* x, int64_t ld_x, void* out, float* inv_scale, int rows,
+                                 int cols, hipStream_t s);
+
 // ---------------------------------------------------------------- attention
 struct AttnParams {
   const void* q;           // [B][n_kv][r_alloc][hd], pre-scaled by log2(e)/sqrt(hd)
@@ -95,7 +101,8 @@ enum Epilogue {
   kEpiStore = 0,      // C fp32 = acc
   kEpiResidRow = 1,   // C fp32 = acc + R[(m % r_mod) * r_ld + n]   (R in the storage dtype)
   kEpiResidF32 = 2,   // C fp32 = acc + R[m * r_ld + n]   (R fp32; r_ld 0 = one row for all m)
-  kEpiSwiglu = 3      // C (activation dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
+  kEpiSwiglu = 3,     // C (activation dtype) [m][n] = silu(acc_gate) * acc_up, n < N/2
+  kEpiRowScale = 4    // C fp32 = acc * R[m]               (R fp32, one factor per row)
 };
 struct GemmParams {
   const void* a;           // [M][lda], activation dtype (fp16 for bf16 storage)
@@ -116,6 +123,8 @@ struct ClsParams {
   const void* final_norm;  // [d]
   const void* w_cls;       // [n_tasks][C][d]
   const float* b_cls;      // nullable, [n_tasks][C]
+  const int* cls_rows;     // nullable, [n_tasks][C]: row of w_cls (a vocabulary matrix) per class
+  const int* err;          // nullable: skip everything if *err != 0
   float* logits;           // [B][n_tasks][C]
   int k, d, n_classes, pool_mean, n_tasks;
   float eps;
@@ -129,6 +138,9 @@ struct ValidateParams {
   int* err;
   int64_t num_blocks;
   int mbps, bs_log2, max_seq_len;
+  const int* cls_rows;     // nullable: n_cls_rows row indices, each < cls_vocab
+  int n_cls_rows;
+  int64_t cls_vocab;
 };
 hipError_t launch_validate(const ValidateParams& p, int batch, hipStream_t s);
 

@@ -160,10 +160,11 @@ template <typename T>
 __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
   __shared__ float red[4];
   const int b = blockIdx.x, tc = blockIdx.y, d = p.d;  // tc = task * C + class
+  if (p.err && *p.err) return;
   const int task = tc / p.n_classes;
   const int j0 = p.pool_mean ? 0 : p.k - 1;
   const float w = p.pool_mean ? 1.0f / (float)p.k : 1.0f;
-  const T* wr = (const T*)p.w_cls + (int64_t)tc * d;
+  const T* wr = (const T*)p.w_cls + (p.cls_rows ? (int64_t)p.cls_rows[tc] : (int64_t)tc) * d;
   const T* gm = (const T*)p.final_norm;
   float wg[kRowChunks][4];  // W_cls[c][i] * gamma_i, reused for every row
 #pragma unroll
@@ -202,9 +203,37 @@ __global__ __launch_bounds__(256) void final_classifier(const ClsParams p) {
     p.logits[(int64_t)b * p.n_tasks * p.n_classes + tc] = logit + (p.b_cls ? p.b_cls[tc] : 0.f);
 }
 
+// ---------------------------------------------------------------- fp16 staging with row scales
+// One workgroup per row: max |x| over the row, then the scaled fp16 copy.
+__global__ __launch_bounds__(256) void scale_rows_f16(const bf16* x, int64_t ld_x, f16* out,
+                                                      float* inv_scale, int cols) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const bf16* xr = x + (int64_t)r * ld_x;
+  float mx = 0.f;
+  for (int i = threadIdx.x; i < cols; i += 256) mx = fmaxf(mx, fabsf(to_f32(xr[i])));
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  int e = 0;
+  while (e < 126 && ldexpf(mx, -e) >= 32768.0f) ++e;
+  const float sc = ldexpf(1.0f, -e);
+  f16* orow = out + (int64_t)r * cols;
+  for (int i = threadIdx.x; i < cols; i += 256) orow[i] = (f16)(to_f32(xr[i]) * sc);
+  if (threadIdx.x == 0) inv_scale[r] = ldexpf(1.0f, e);
+}
+
 // ---------------------------------------------------------------- validation
 __global__ void validate_meta(const ValidateParams p) {
   const int b = blockIdx.x;
+  if (b == 0 && p.cls_rows) {
+    for (int i = threadIdx.x; i < p.n_cls_rows; i += blockDim.x) {
+      const int r = p.cls_rows[i];
+      if (r < 0 || (int64_t)r >= p.cls_vocab) atomicOr(p.err, 8);
+    }
+  }
   const int n = p.seq_lens[b];
   if (n < 0 || n > p.max_seq_len) {
     if (threadIdx.x == 0) atomicOr(p.err, 1);
@@ -253,6 +282,14 @@ hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStre
     hipLaunchKernelGGL((rope_scatter<float, false>), grid, block, 0, s, p);
   else
     return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_rows_f16(const void* x, int64_t ld_x, void* out, float* inv_scale, int rows,
+                                 int cols, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(scale_rows_f16, dim3(rows), dim3(256), 0, s, (const bf16*)x, ld_x, (f16*)out,
+                     inv_scale, cols);
   return hipGetLastError();
 }
 

@@ -46,7 +46,7 @@ struct Plan {
   // recursive steps only: per-sequence queries and soft keys/values, the fused
   // rows and their inputs
   size_t off_rq, off_rq_lo, off_rks, off_rks_lo, off_rvs, off_rvs_lo, off_rqkv, off_ru, off_rhn,
-      off_ren, off_rce, off_rx;
+      off_ren, off_rce, off_rx, off_r3, off_rh0, off_rscale;
   size_t total;
 };
 
@@ -195,6 +195,10 @@ Plan make_plan(const sp_probe_config& c) {
   p.off_ren = take((size_t)c.k * d * e);
   p.off_rce = take((size_t)c.k * d * 4);
   p.off_rx = take(Mr * d * 4);
+  // Eagle3 input: the three hidden states as scaled fp16 rows, the projected first hidden state
+  p.off_r3 = take(B * 3 * d * e);
+  p.off_rh0 = take(B * d * 4);
+  p.off_rscale = take(B * 4);
   p.total = o;
   return p;
 }
@@ -263,6 +267,7 @@ int check_forward(const sp_probe* h, const sp_kv_cache* kv, const int32_t* seq_l
   for (const void* q : wptr)
     if (!q || !aligned16(q)) return SP_ERR_INVALID_ARG;
   if (!aligned16(soft_prompt)) return SP_ERR_INVALID_ARG;
+  if (wt->cls_rows && (wt->cls_vocab < 1 || ((uintptr_t)wt->cls_rows & 3))) return SP_ERR_INVALID_ARG;
   if (!kv->k_base || !kv->v_base || !aligned16(kv->k_base) || !aligned16(kv->v_base))
     return SP_ERR_INVALID_ARG;
   if (kv->block_size < 16 || !is_pow2(kv->block_size) || kv->max_blocks_per_seq < 1 ||
@@ -468,7 +473,7 @@ int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_le
 
   if (debug) {
     ValidateParams vp{seq_lens, block_table, err, kv->num_blocks, kv->max_blocks_per_seq,
-                      ilog2(kv->block_size), c.max_seq_len};
+                      ilog2(kv->block_size), c.max_seq_len, wt->cls_rows, n_tasks * c.n_classes, wt->cls_vocab};
     SP_TRY(launch_validate(vp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
@@ -558,6 +563,7 @@ int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_le
     ClsParams cp{};
     cp.y = at<float>(h, pl.off_y);
     cp.final_norm = wt->final_norm; cp.w_cls = wt->w_cls; cp.b_cls = wt->b_cls;
+    cp.cls_rows = wt->cls_rows; cp.err = errp;
     cp.logits = logits;
     cp.k = Kq; cp.n_tasks = n_tasks; cp.d = d; cp.n_classes = c.n_classes;
     cp.pool_mean = c.pool == SP_POOL_MEAN;
@@ -595,6 +601,8 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
   const void* fptr[3] = {fusion->fc_norm_hidden, fusion->fc_norm_embed, fusion->w_fc};
   for (const void* q : fptr)
     if (!q || !aligned16(q)) return SP_ERR_INVALID_ARG;
+  const bool eagle3 = fusion->w_hidden_fuse != nullptr;
+  if (eagle3 && !aligned16(fusion->w_hidden_fuse)) return SP_ERR_INVALID_ARG;
   const sp_probe_config& c = h->cfg;
   const Plan& pl = h->plan;
   const AttnPlan& rp = pl.rec;
@@ -623,7 +631,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
 
   if (debug) {
     ValidateParams vp{seq_lens, block_table, err, kv->num_blocks, kv->max_blocks_per_seq,
-                      ilog2(kv->block_size), c.max_seq_len};
+                      ilog2(kv->block_size), c.max_seq_len, wt->cls_rows, c.n_classes, wt->cls_vocab};
     SP_TRY(launch_validate(vp, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
@@ -634,9 +642,28 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
                              at<void>(h, pl.off_ren), d, K, d, c.rms_eps, s));
   SP_TRY(launch_gemm(dt, kEpiStore, gemm_one(at<void>(h, pl.off_ren), d, w_fc_embed, 2 * d,
                                              at<void>(h, pl.off_rce), d, K, d, d), s));
-  // the first step's hidden state is the base model's last one
-  SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, hidden_last, d, fusion->fc_norm_hidden, nullptr, hn, d,
-                             B, d, c.rms_eps, s));
+  if (!eagle3) {
+    // the first step's hidden state is the base model's last one
+    SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, hidden_last, d, fusion->fc_norm_hidden, nullptr, hn, d,
+                               B, d, c.rms_eps, s));
+  } else {
+    // Eagle3: the first step's hidden state is W [h_low; h_mid; h_high]; on the
+    // bf16 path the three states enter the MFMA as fp16 rows scaled by a power
+    // of two (their range can exceed fp16's) and the product is scaled back
+    float* h0 = at<float>(h, pl.off_rh0);
+    if (dt == kBF16) {
+      SP_TRY(launch_scale_rows_f16(hidden_last, 3 * d, at<void>(h, pl.off_r3), at<float>(h, pl.off_rscale),
+                                   B, 3 * d, s));
+      GemmParams g = gemm_one(at<void>(h, pl.off_r3), 3 * d, fusion->w_hidden_fuse, 3 * d, h0, d, B, d, 3 * d);
+      g.r = at<float>(h, pl.off_rscale);
+      SP_TRY(launch_gemm(dt, kEpiRowScale, g, s));
+    } else {
+      SP_TRY(launch_gemm(dt, kEpiStore, gemm_one(hidden_last, 3 * d, fusion->w_hidden_fuse, 3 * d, h0, d,
+                                                 B, d, 3 * d), s));
+    }
+    SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, h0, d, fusion->fc_norm_hidden, nullptr, hn, d, B, d,
+                               c.rms_eps, s));
+  }
 
   for (int t = 0; t < K; ++t) {
     // stage 0: x_t = W_fc[:, :d] RMSNorm(h; gamma_h) + c_t, its RMSNorm, Q/K/V, RoPE at N_b + t
@@ -734,6 +761,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       ClsParams cp{};
       cp.y = (const float*)y_all;
       cp.final_norm = wt->final_norm; cp.w_cls = wt->w_cls; cp.b_cls = wt->b_cls;
+      cp.cls_rows = wt->cls_rows; cp.err = errp;
       cp.logits = logits;
       cp.k = K; cp.n_tasks = 1; cp.d = d; cp.n_classes = c.n_classes;
       cp.pool_mean = c.pool == SP_POOL_MEAN;

@@ -33,7 +33,7 @@ _TAGS = {
     "seq_len": 1, "perm": 2, "kv": 3, "soft": 10, "in_norm": 11, "w_q": 12, "w_k": 13, "w_v": 14,
     "w_o": 15, "post_norm": 16, "w_gate": 17, "w_up": 18, "w_down": 19, "final_norm": 20,
     "w_cls": 21, "b_cls": 22, "fc_norm_hidden": 23, "fc_norm_embed": 24, "w_fc": 25,
-    "hidden_last": 26,
+    "hidden_last": 26, "lm_head": 27, "cls_rows": 28, "w_hidden_fuse": 29, "hidden3": 30,
 }
 
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
@@ -135,6 +135,32 @@ def fusion_params(w: Workload, device="cpu") -> dict:
         "w_fc": _normal((d, 2 * d), 0.0, w.weight_std, dt, device, _gen(w, "w_fc", device)),
         "hidden_last": _normal((w.batch, d), 0.0, 1.0, dt, device, _gen(w, "hidden_last", device)),
     }
+
+
+def lm_head_params(w: Workload, vocab: int, n_tasks: int = 1, device="cpu") -> dict:
+    """Vocabulary read-out inputs: a frozen LM head [vocab][d] ~ N(0, weight_std^2) in
+    the storage dtype and, per task, C distinct label-token rows (int32 [T][C])."""
+    dt = TORCH_DTYPE[w.dtype]
+    head = _normal((vocab, w.hidden), 0.0, w.weight_std, dt, device, _gen(w, "lm_head", device))
+    rng = np.random.default_rng(_seed(w, "cls_rows"))
+    rows = np.stack([rng.choice(vocab, w.n_classes, replace=False) for _ in range(n_tasks)]).astype(np.int32)
+    return {"lm_head": head, "cls_rows": torch.from_numpy(rows).to(device)}
+
+
+def eagle3_params(w: Workload, device="cpu") -> dict:
+    """Eagle3 input: the projection w_hidden_fuse [d][3d] ~ N(0, weight_std^2) and three
+    base-model hidden states per sequence, hidden3 [B][3d] ~ N(0, 1), with a few
+    large entries per state (magnitudes up to 1e5, as base models' massive
+    activations can be; beyond fp16's range on purpose)."""
+    dt = TORCH_DTYPE[w.dtype]
+    d = w.hidden
+    wf = _normal((d, 3 * d), 0.0, w.weight_std, dt, device, _gen(w, "w_hidden_fuse", device))
+    g = _gen(w, "hidden3", device)
+    h = torch.randn((w.batch, 3 * d), generator=g, device=device, dtype=torch.float32)
+    idx = torch.randint(0, 3 * d, (w.batch, 4), generator=g, device=device)
+    big = torch.tensor([3.0e3, -2.0e4, 1.0e5, 600.0], device=device).expand(w.batch, 4)
+    h.scatter_(1, idx, big)
+    return {"w_hidden_fuse": wf, "hidden3": h.to(dt)}
 
 
 @dataclass

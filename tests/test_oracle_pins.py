@@ -347,3 +347,32 @@ def test_tasks_are_independent_probes():
     np.testing.assert_array_equal(out2[:, 2], out[:, 2])
     perm = [2, 0, 1]
     np.testing.assert_array_equal(O.probe_batch_tasks(kvs, soft[perm], wc[perm], bc[perm], W, hs), out[:, perm])
+
+
+def test_lm_head_readout_reads_only_the_label_rows():
+    """Sec. 6.7 / Table 7: the frozen-LM-head read-out scores the pooled state with
+    the rows of the label tokens only.  It equals the linear head made of those
+    rows; the other vocabulary rows have no effect; swapping the two labels
+    negates the yes/no score."""
+    rng = np.random.default_rng(61)
+    d, n_q, n_kv, hd, inter, k, V = 16, 4, 2, 4, 20, 3, 50
+    W = rand_weights(rng, d, n_q, n_kv, hd, inter, 2)
+    vocab = rng.standard_normal((V, d))
+    kc, vc = rng.standard_normal((2, n_kv, 6, hd))
+    soft = rng.standard_normal((k, d))
+    hs = O.HeadShape(n_q, n_kv, hd)
+    yes, no = 17, 42
+    lm = O.probe_sequence(kc, vc, soft, dict(W, w_cls=vocab, cls_rows=[yes, no]), hs)
+    lin = O.probe_sequence(kc, vc, soft, dict(W, w_cls=vocab[[yes, no]]), hs)
+    np.testing.assert_array_equal(lm["logits"], lin["logits"])
+    other = vocab.copy()
+    other[[i for i in range(V) if i not in (yes, no)]] *= -3.0
+    np.testing.assert_array_equal(
+        O.probe_sequence(kc, vc, soft, dict(W, w_cls=other, cls_rows=[yes, no]), hs)["logits"], lm["logits"])
+    sw = O.probe_sequence(kc, vc, soft, dict(W, w_cls=vocab, cls_rows=[no, yes]), hs)["logits"]
+    assert sw[0] - sw[1] == -(lm["logits"][0] - lm["logits"][1])
+    # tasks reading different rows of one shared vocabulary matrix
+    rows = np.array([[yes, no], [3, 4]])
+    out = O.probe_batch_tasks([(kc, vc)], np.stack([soft, soft]), vocab, None, W, hs, cls_rows=rows)
+    np.testing.assert_array_equal(out[0, 0], lm["logits"])
+    np.testing.assert_array_equal(out[0, 1], O.probe_sequence(kc, vc, soft, dict(W, w_cls=vocab[[3, 4]]), hs)["logits"])

@@ -147,3 +147,26 @@ def test_batch_is_a_loop_over_sequences():
     for b in range(3):
         one = O.probe_sequence_recursive(kvs[b][0], kvs[b][1], e, h[b], W, hs)["logits"]
         np.testing.assert_array_equal(one, logits[b])
+
+
+def test_eagle3_input_selects_and_scales():
+    """Sec. 3.1 (Eagle3): the first hidden state is a projection of three base-model
+    hidden states.  Selecting one of them ([0 | 0 | I], [I | 0 | 0]) is the MTP
+    recursion on that state; with eps = 0 a positive common scale of the three
+    states changes nothing (they enter through RMSNorm after a linear map)."""
+    shape = (16, 4, 2, 4, 24, 3, 6)
+    d, n_q, n_kv, hd, inter, k, N = shape
+    W, x_ctx, e, h_last, kc, vc = setup(shape, 43)
+    rng = np.random.default_rng(44)
+    h3 = rng.standard_normal((3, d))
+    hs = O.HeadShape(n_q, n_kv, hd, 1e-6, 10000.0, "mean")
+    Z, I = np.zeros((d, d)), np.eye(d)
+    for sel, blocks in ((2, [Z, Z, I]), (0, [I, Z, Z])):
+        got = O.probe_sequence_recursive(kc, vc, e, h3.reshape(-1), dict(W, w_hidden_fuse=np.concatenate(blocks, 1)), hs)
+        ref = ind.draft_without_cache(x_ctx, e, h3[sel], W, n_q, n_kv, hd, 1e-6, 10000.0)
+        np.testing.assert_allclose(got["f"], ref["f"], rtol=0, atol=1e-12)
+    hs0 = O.HeadShape(n_q, n_kv, hd, 0.0, 10000.0, "mean")
+    Wf = dict(W, w_hidden_fuse=0.3 * rng.standard_normal((d, 3 * d)))
+    a = O.probe_sequence_recursive(kc, vc, e, h3.reshape(-1), Wf, hs0)
+    b = O.probe_sequence_recursive(kc, vc, e, 250.0 * h3.reshape(-1), Wf, hs0)
+    np.testing.assert_allclose(b["logits"], a["logits"], rtol=0, atol=1e-11)
