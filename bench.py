@@ -72,9 +72,10 @@ def traffic_per_launch(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, kv, params, seconds: float, fusion=None):
+def cpu_baseline(w, kv, params, seconds: float, fusion=None, tasks=None):
     """The oracle, as written, timed on the host over whole sequences of the
-    workload (the recursive oracle when fusion inputs are given)."""
+    workload (the recursive oracle when fusion inputs are given; every task's
+    probe per sequence when tasks are given)."""
     import numpy as np
     import threadpoolctl
 
@@ -93,19 +94,24 @@ def cpu_baseline(w, kv, params, seconds: float, fusion=None):
         k, v = kv.logical_kv(b)
         k, v = k.double().cpu().numpy(), v.double().cpu().numpy()
         t = time.perf_counter()
-        if fusion is None:
-            oracle.probe_sequence(k, v, soft, W, shape)
-        else:
+        if fusion is not None:
             oracle.probe_sequence_recursive(k, v, soft, h_last[b], W, shape)
+        elif tasks is not None:
+            f = lambda x: None if x is None else x.double().cpu().numpy()
+            oracle.probe_batch_tasks([(k, v)], f(tasks["soft_prompts"]), f(tasks["w_cls"]),
+                                     f(tasks["b_cls"]), W, shape)
+        else:
+            oracle.probe_sequence(k, v, soft, W, shape)
         spent += time.perf_counter() - t
         done += 1
         toks += k.shape[1]
         del k, v
         if spent >= seconds:
             break
-    return {"value": done / spent, "unit": "classifications/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} of {w.batch} sequences ({toks} context tokens), fp64 numpy, "
-                      f"{spent:.1f} s"}
+    n_tasks = 1 if tasks is None else tasks["soft_prompts"].shape[0]
+    return {"value": done * n_tasks / spent, "unit": "classifications/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} of {w.batch} sequences ({toks} context tokens) x {n_tasks} task(s), "
+                      f"fp64 numpy, {spent:.1f} s"}
 
 
 def main():
@@ -202,7 +208,7 @@ def main():
     probe.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds, fusion)
+        out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds, fusion, tasks)
     print(json.dumps(out), flush=True)
 
 

@@ -14,6 +14,10 @@
 // 16-byte bank groups.
 // SwiGLU: the BN weight rows of a tile alternate 16 gate rows and the 16
 // matching up rows, so every lane holds gate and up of the same outputs.
+// Split-K (PART, small M: the product then streams the weights with too few
+// workgroups to keep enough loads in flight): blockIdx.y takes a slice of the
+// K steps and writes its fp32 partial tile; gemm_reduce sums the slices in a
+// fixed order and applies the epilogue.
 #include "common.h"
 #include "kernels.h"
 
@@ -22,7 +26,7 @@ namespace {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int BM, int BN, int WGM, int WGN, int S, int BK, int EPI>
+template <int BM, int BN, int WGM, int WGN, int S, int BK, int EPI, bool PART = false>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   constexpr int NW = WGM * WGN, WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
   constexpr int PPR = BK / 8;                        // 16-byte pieces per tile row
@@ -107,13 +111,15 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   // Steps past the last re-load the last one (into a stage no later step
   // reads), so every step issues the same loads and one vmcnt value fits all.
   const int KT = p.K / BK;
+  const int kb = (int)(((int64_t)KT * blockIdx.y) / gridDim.y);       // this slice's K steps
+  const int ke = (int)(((int64_t)KT * (blockIdx.y + 1)) / gridDim.y);
 #pragma unroll
-  for (int st = 0; st < S - 1; ++st) issue(min(st, KT - 1), st);
+  for (int st = 0; st < S - 1; ++st) issue(min(kb + st, ke - 1), st);
   int stg = 0;
-  for (int kt = 0; kt < KT; ++kt) {
+  for (int kt = kb; kt < ke; ++kt) {
     wait_vmcnt<(S - 2) * IPW>();  // this wave's loads of step kt have landed
     lds_barrier();                // everyone's have; everyone is done with step kt - 1
-    issue(min(kt + S - 1, KT - 1), stg == 0 ? S - 1 : stg - 1);
+    issue(min(kt + S - 1, ke - 1), stg == 0 ? S - 1 : stg - 1);
     const u32x4* As = lds + stg * STAGE;
     const u32x4* Bs = As + BM * PPR;
 #pragma unroll
@@ -142,7 +148,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
     for (int r = 0; r < 4; ++r) {
       const int m = m0 + wm * WM + 16 * i + 4 * la + r;
       if (m >= p.M) continue;
-      if (EPI == kEpiSwiglu) {
+      if (PART) {
+        float* prow = p.part + ((int64_t)blockIdx.y * p.M + m) * p.N + n0 + wn * WN + li;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) prow[16 * j] = acc[i][j][r];
+      } else if (EPI == kEpiSwiglu) {
 #pragma unroll
         for (int j = 0; j < NT; j += 2) {
           const int pair = (wn * WN + 16 * j) >> 5;
@@ -201,6 +211,58 @@ __global__ __launch_bounds__(256) void gemm_f32(const GemmParams p) {
   ((float*)p.c)[(int64_t)m * p.ldc + n] = acc;
 }
 
+// Sum of the split-K slices and the epilogue, one thread per output.  SwiGLU:
+// output o of tile o / (bn/2) has its gate column 32 ((o % (bn/2)) / 16) +
+// o % 16 in the tile's interleaved columns and its up column 16 later.
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_reduce(const GemmParams p, int ksplit, int bn) {
+  const int n_out = EPI == kEpiSwiglu ? p.N / 2 : p.N;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)p.M * n_out) return;
+  const int m = (int)(idx / n_out), o = (int)(idx % n_out);
+  const int64_t slice = (int64_t)p.M * p.N;
+  const float* src = p.part + (int64_t)m * p.N;
+  if (EPI == kEpiSwiglu) {
+    const int w = o % (bn / 2);
+    const int g = (o / (bn / 2)) * bn + 32 * (w / 16) + w % 16;
+    float gt = 0.f, up = 0.f;
+    for (int k = 0; k < ksplit; ++k) {
+      gt += src[k * slice + g];
+      up += src[k * slice + g + 16];
+    }
+    ((f16*)p.c)[(int64_t)m * p.ldc + o] = (f16)(silu(gt) * up);
+    return;
+  }
+  float v = 0.f;
+  for (int k = 0; k < ksplit; ++k) v += src[k * slice + o];
+  if (EPI == kEpiResidRow) v += (float)((const bf16*)p.r)[(int64_t)(m % p.r_mod) * p.r_ld + o];
+  if (EPI == kEpiResidF32) v += ((const float*)p.r)[(int64_t)m * p.r_ld + o];
+  if (EPI == kEpiRowScale) v *= ((const float*)p.r)[m];
+  ((float*)p.c)[(int64_t)m * p.ldc + o] = v;
+}
+
+template <int BM, int BN, int WGM, int WGN, int S, int BK>
+hipError_t launch_split(Epilogue epi, const GemmParams& p, int ksplit, hipStream_t s) {
+  const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN), ksplit), block(64 * WGM * WGN);
+  switch (epi) {
+    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore, true>), grid, block, 0, s, p); break;
+    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow, true>), grid, block, 0, s, p); break;
+    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32, true>), grid, block, 0, s, p); break;
+    case kEpiRowScale: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiRowScale, true>), grid, block, 0, s, p); break;
+    case kEpiSwiglu: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu, true>), grid, block, 0, s, p); break;
+  }
+  const int n_out = epi == kEpiSwiglu ? p.N / 2 : p.N;
+  const dim3 rgrid((unsigned)(((int64_t)p.M * n_out + 255) / 256));
+  switch (epi) {
+    case kEpiStore: hipLaunchKernelGGL(gemm_reduce<kEpiStore>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
+    case kEpiResidRow: hipLaunchKernelGGL(gemm_reduce<kEpiResidRow>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
+    case kEpiResidF32: hipLaunchKernelGGL(gemm_reduce<kEpiResidF32>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
+    case kEpiRowScale: hipLaunchKernelGGL(gemm_reduce<kEpiRowScale>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
+    case kEpiSwiglu: hipLaunchKernelGGL(gemm_reduce<kEpiSwiglu>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
+  }
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int WGM, int WGN, int S, int BK>
 hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
   if (p.K % BK) return hipErrorInvalidValue;
@@ -251,6 +313,27 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     return hipGetLastError();
   }
   if (p.K % 32 || p.lda % 8 || p.ldb % 8) return hipErrorInvalidValue;
+  // 17..32 rows: the product streams the weights; a 32-row by 128-column tile
+  // with four waves, and K split so that the grid has enough workgroups in
+  // flight (each slice at least 8 steps of 64).  (Up to 16 rows the one-wave
+  // 16-row tiles below measured faster.)
+  constexpr TileShape kSmall{32, 128, 1, 4, 64};
+  if (p.M > 16 && p.M <= 32 && tile_ok(p, epi, kSmall)) {
+    const int tiles = p.N / 128, KT = p.K / 64;
+    int ks = 1;
+    while (ks < 16 && tiles * ks * 2 <= 1024 && KT / (ks * 2) >= 8 &&
+           (size_t)(ks * 2) * p.M * p.N * sizeof(float) <= p.part_bytes && p.part)
+      ks *= 2;
+    if (ks > 1) return launch_split<32, 128, 1, 4, 6, 64>(epi, p, ks, s);
+    return launch_lds_tile<32, 128, 1, 4, 6, 64>(epi, p, s);
+  }
+  // Long K with a few hundred rows (the down projection of 512 rows): 256 x 128
+  // tiles with K split four ways re-read the activations and weights half as
+  // often as the 128 x 64 tiles, at the same workgroup count.
+  constexpr TileShape kLongK{256, 128, 4, 2, 64};
+  if (p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kLongK) && p.part &&
+      (size_t)4 * p.M * p.N * sizeof(float) <= p.part_bytes)
+    return launch_split<256, 128, 4, 2, 3, 64>(epi, p, 4, s);
   // First tile (in preference order) that gives at least one workgroup per
   // compute unit (256), else the valid tile with the most workgroups.
   int best = -1;

@@ -113,6 +113,10 @@ struct GemmParams {
   void* c;
   const void* r;           // residual
   int M, N, K, lda, ldc, r_mod, r_ld;
+  // nullable scratch for split-K partial sums of small-M products (fp32); the
+  // launcher splits K only when the partials fit in part_bytes
+  float* part;
+  size_t part_bytes;
 };
 // dt: storage dtype of the weights (kF32: fp32 VALU path; kBF16: fp16 MFMA path)
 hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s);

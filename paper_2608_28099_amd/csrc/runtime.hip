@@ -47,6 +47,7 @@ struct Plan {
   // rows and their inputs
   size_t off_rq, off_rq_lo, off_rks, off_rks_lo, off_rvs, off_rvs_lo, off_rqkv, off_ru, off_rhn,
       off_ren, off_rce, off_rx, off_r3, off_rh0, off_rscale;
+  size_t off_gpart, gpart_bytes;  // split-K partial sums of the small-row projections
   size_t total;
 };
 
@@ -199,6 +200,9 @@ Plan make_plan(const sp_probe_config& c) {
   p.off_r3 = take(B * 3 * d * e);
   p.off_rh0 = take(B * d * 4);
   p.off_rscale = take(B * 4);
+  const size_t widest = std::max({(size_t)2 * c.intermediate, (size_t)p.nqkv, d});
+  p.gpart_bytes = 16 * 32 * widest * 4;
+  p.off_gpart = take(p.gpart_bytes);
   p.total = o;
   return p;
 }
@@ -248,6 +252,13 @@ hipEvent_t* prof_begin(sp_probe* h, int marks) {
 void prof_commit(sp_probe* h, int marks) {
   h->records.push_back({h->cursor, marks});
   h->cursor += marks;
+}
+
+// A projection with the handle's split-K scratch.
+hipError_t run_gemm(sp_probe* h, DType dt, Epilogue epi, GemmParams g, hipStream_t s) {
+  g.part = at<float>(h, h->plan.off_gpart);
+  g.part_bytes = h->plan.gpart_bytes;
+  return launch_gemm(dt, epi, g, s);
 }
 
 // Host-side checks shared by the forwards; *noop is set for an empty batch.
@@ -481,7 +492,7 @@ int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_le
   // stage 0: soft rows — RMSNorm, Q/K/V on the S distinct rows, RoPE per sequence
   SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, d, wt->in_norm, nullptr,
                              at<void>(h, pl.off_u), d, S, d, c.rms_eps, s));
-  SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_u), at<void>(h, pl.off_qkv), S), s));
+  SP_TRY(run_gemm(h, dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_u), at<void>(h, pl.off_qkv), S), s));
   {
     RopeParams r{};
     r.qkv = at<float>(h, pl.off_qkv);
@@ -537,7 +548,7 @@ int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_le
     g.r = (const char*)soft_prompt + (size_t)(K - Kq) * d * pl.esz;
     g.r_mod = R;
     g.r_ld = last_only ? K * d : d;
-    SP_TRY(launch_gemm(dt, kEpiResidRow, g, s));
+    SP_TRY(run_gemm(h, dt, kEpiResidRow, g, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
@@ -547,14 +558,14 @@ int forward_one_pass(sp_probe_t* h, const sp_kv_cache* kv, const int32_t* seq_le
   if (!mark()) return SP_ERR_HIP;
 
   // stage 5: s = silu(W_gate w) * (W_up w)
-  SP_TRY(launch_gemm(dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), M), s));
+  SP_TRY(run_gemm(h, dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), M), s));
   if (!mark()) return SP_ERR_HIP;
 
   // stage 6: y = a + W_down s
   {
     GemmParams g = gemm_one(at<void>(h, pl.off_s), I, wt->w_down, I, at<void>(h, pl.off_y), d, M, d, I);
     g.r = at<void>(h, pl.off_a); g.r_ld = d;
-    SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+    SP_TRY(run_gemm(h, dt, kEpiResidF32, g, s));
   }
   if (!mark()) return SP_ERR_HIP;
 
@@ -640,7 +651,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
   // c_t = W_fc[:, d:] RMSNorm(e_t; gamma_e) for the k steps, once.
   SP_TRY(launch_rmsnorm_rows(dt, dt, at_dt, soft_prompt, d, fusion->fc_norm_embed, nullptr,
                              at<void>(h, pl.off_ren), d, K, d, c.rms_eps, s));
-  SP_TRY(launch_gemm(dt, kEpiStore, gemm_one(at<void>(h, pl.off_ren), d, w_fc_embed, 2 * d,
+  SP_TRY(run_gemm(h, dt, kEpiStore, gemm_one(at<void>(h, pl.off_ren), d, w_fc_embed, 2 * d,
                                              at<void>(h, pl.off_rce), d, K, d, d), s));
   if (!eagle3) {
     // the first step's hidden state is the base model's last one
@@ -656,9 +667,9 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
                                    B, 3 * d, s));
       GemmParams g = gemm_one(at<void>(h, pl.off_r3), 3 * d, fusion->w_hidden_fuse, 3 * d, h0, d, B, d, 3 * d);
       g.r = at<float>(h, pl.off_rscale);
-      SP_TRY(launch_gemm(dt, kEpiRowScale, g, s));
+      SP_TRY(run_gemm(h, dt, kEpiRowScale, g, s));
     } else {
-      SP_TRY(launch_gemm(dt, kEpiStore, gemm_one(hidden_last, 3 * d, fusion->w_hidden_fuse, 3 * d, h0, d,
+      SP_TRY(run_gemm(h, dt, kEpiStore, gemm_one(hidden_last, 3 * d, fusion->w_hidden_fuse, 3 * d, h0, d,
                                                  B, d, 3 * d), s));
     }
     SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, h0, d, fusion->fc_norm_hidden, nullptr, hn, d, B, d,
@@ -671,11 +682,11 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       GemmParams g = gemm_one(hn, d, fusion->w_fc, 2 * d, x_all + (size_t)t * d * 4, (int)ld_steps,
                               B, d, d);
       g.r = at<char>(h, pl.off_rce) + (size_t)t * d * 4; g.r_ld = 0;
-      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+      SP_TRY(run_gemm(h, dt, kEpiResidF32, g, s));
     }
     SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, x_all + (size_t)t * d * 4, ld_steps, wt->in_norm,
                                nullptr, at<void>(h, pl.off_ru), d, B, d, c.rms_eps, s));
-    SP_TRY(launch_gemm(dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_ru), at<void>(h, pl.off_rqkv), B), s));
+    SP_TRY(run_gemm(h, dt, kEpiStore, gemm_qkv(c, pl, wt, at<void>(h, pl.off_ru), at<void>(h, pl.off_rqkv), B), s));
     {
       RopeParams r{};
       r.qkv = at<float>(h, pl.off_rqkv);
@@ -729,7 +740,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       GemmParams g = gemm_one(o_all + (size_t)t * qw * esz, K * qw, wt->w_o, qw,
                               a_all + (size_t)t * d * 4, (int)ld_steps, B, d, qw);
       g.r = x_all + (size_t)t * d * 4; g.r_ld = (int)ld_steps;
-      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+      SP_TRY(run_gemm(h, dt, kEpiResidF32, g, s));
     }
     if (!mark()) return SP_ERR_HIP;
 
@@ -739,7 +750,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
     if (!mark()) return SP_ERR_HIP;
 
     // stage 5: s = silu(W_gate w) * (W_up w)
-    SP_TRY(launch_gemm(dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), B), s));
+    SP_TRY(run_gemm(h, dt, kEpiSwiglu, gemm_gate_up(c, wt, at<void>(h, pl.off_w), at<void>(h, pl.off_s), B), s));
     if (!mark()) return SP_ERR_HIP;
 
     // stage 6: y_t = a_t + W_down s
@@ -747,7 +758,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       GemmParams g = gemm_one(at<void>(h, pl.off_s), I, wt->w_down, I, y_all + (size_t)t * d * 4,
                               (int)ld_steps, B, d, I);
       g.r = a_all + (size_t)t * d * 4; g.r_ld = (int)ld_steps;
-      SP_TRY(launch_gemm(dt, kEpiResidF32, g, s));
+      SP_TRY(run_gemm(h, dt, kEpiResidF32, g, s));
     }
     if (!mark()) return SP_ERR_HIP;
 

@@ -130,8 +130,9 @@ def test_head_dims_and_splits(hd, dev):
 
 def test_projection_tile_shapes(dev):
     """Shapes whose projections select the fallback tiles of the bf16 GEMM:
-    64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, and the
-    32-deep K step (width 4128 is not a multiple of 64) with head_dim 64."""
+    64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, the
+    32-deep K step (width 4128 is not a multiple of 64) with head_dim 64, and
+    the split-K 256x128 tile of a deep down projection."""
     cases = [
         configs.Workload(name="tiles_a", dtype="bf16", batch=16, k=16, hidden=4096, n_q_heads=8,
                          n_kv_heads=2, head_dim=128, intermediate=1024, n_classes=3,
@@ -139,6 +140,10 @@ def test_projection_tile_shapes(dev):
         configs.Workload(name="tiles_b", dtype="bf16", batch=4, k=8, hidden=4128, n_q_heads=4,
                          n_kv_heads=2, head_dim=64, intermediate=512, n_classes=2,
                          seq_len=("list", (257, 64, 0, 33)), seed=51),
+        # 144 rows and a down projection 8192 deep: 256 x 128 tiles with K split four ways
+        configs.Workload(name="tiles_c", dtype="bf16", batch=9, k=16, hidden=512, n_q_heads=8,
+                         n_kv_heads=2, head_dim=64, intermediate=8192, n_classes=2,
+                         seq_len=("uniform", 0, 700), seed=52),
     ]
     for w in cases:
         announce(f"[tiles] {w.name}")

@@ -221,3 +221,25 @@ def test_recursive_full_size_sampled_sequences(w, dev):
     probe.close()
     del kv, params
     torch.cuda.empty_cache()
+
+
+def test_split_k_projections(dev):
+    """Widths at which the projections of 17..32 rows (24 per step here) split K
+    over several workgroups (fusion, Q/K/V, o, gate/up, down), in the recursive
+    form and in the one-pass form with last-row-only execution, against the
+    oracle."""
+    w = configs.Workload(name="split_k_bf16", dtype="bf16", batch=24, k=2, hidden=2048, n_q_heads=16,
+                         n_kv_heads=4, head_dim=128, intermediate=3072, n_classes=3,
+                         seq_len=("uniform", 0, 2100), seed=95)
+    kv, params, fusion, kv_d, p_d, f_d = case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward_recursive(kv_d, p_d, f_d).cpu().numpy()
+    probe.close()
+    err = H.check_logits(got, oracle_logits(w, kv, params, fusion), w.dtype, "recursive")
+    announce(f"[split-k] recursive max err {err:.3e}")
+    probe = binding.Probe(w, flags=binding.SP_FLAG_LAST_ROW_ONLY)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    probe.close()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    err = H.check_logits(got, ref, w.dtype, "last row only")
+    announce(f"[split-k] last-row-only max err {err:.3e}")
