@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "classifications/sec at 1 MI355X; attention KV-read GB/s as % of HBM peak"
 HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix-core peak
 DEFAULT_WORKLOAD = {"one-pass": "long_9b_bf16", "recursive": "long_9b_bf16_sp5"}
 ATTN_SRC = os.path.join(ROOT, "paper_2608_28099_amd", "csrc", "attention.hip")
 PROFILES = os.path.join(ROOT, "profiles")
@@ -72,6 +73,53 @@ def traffic_per_launch(workload: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def projection_rates(w, T, args, recursive, stages, n_fwd):
+    """Achieved MFMA throughput of the projection stages (their algorithmic FLOP
+    over the stage's mean HIP-event time per forward) against the dense peak."""
+    d, I, qkv = w.hidden, w.intermediate, (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim
+    qw = w.n_q_heads * w.head_dim
+    if recursive:   # k steps of B rows each (the fusion's B x d x d product is in soft prep)
+        rows = w.batch * w.k
+    else:
+        rows = w.batch * T * (1 if args.last_row_only else w.k)
+    flop = {"o_proj": 2.0 * rows * d * qw, "gate_up": 2.0 * rows * 2 * I * d, "down": 2.0 * rows * d * I}
+    out = {}
+    for name, f in flop.items():
+        ms = stages[name] / n_fwd
+        tf = f / (ms * 1e-3) / 1e12
+        out[name] = {"gflop": round(f / 1e9, 2), "ms": round(ms, 4), "tflops": round(tf, 1),
+                     "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4)}
+    return out
+
+
+def copy_rate(torch, dev):
+    """Device-to-device copy of 1 GiB (bytes read + written per second): the
+    streaming rate HBM sustains for a plain copy on this machine, for context."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(5):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    rate = 5 * 2 * n / (a.elapsed_time(b) * 1e-3) / 1e9
+    del src, dst
+    return round(rate, 1)
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, kv, params, seconds: float, fusion=None, tasks=None):
     """The oracle, as written, timed on the host over whole sequences of the
     workload (the recursive oracle when fusion inputs are given; every task's
@@ -110,6 +158,7 @@ def cpu_baseline(w, kv, params, seconds: float, fusion=None, tasks=None):
             break
     n_tasks = 1 if tasks is None else tasks["soft_prompts"].shape[0]
     return {"value": done * n_tasks / spent, "unit": "classifications/s", "cores": threads, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": f"{done} of {w.batch} sequences ({toks} context tokens) x {n_tasks} task(s), "
                       f"fp64 numpy, {spent:.1f} s"}
 
@@ -204,6 +253,8 @@ def main():
         "roofline": roofline,
         "attention_gbps": round(achieved, 1),
         "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},
+        "projections": projection_rates(w, T, args, recursive, stages, n_fwd),
+        "hbm_copy_gbps": copy_rate(torch, dev),
     }
     probe.close()
     if not args.no_cpu_baseline:
