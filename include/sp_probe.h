@@ -62,7 +62,7 @@ typedef enum sp_pool {
   SP_POOL_LAST = 0,  /* classify the final-normed hidden state of the last soft row
                         (the read-out of the k-th step, Sec. 3.2) */
   SP_POOL_MEAN = 1   /* mean of the final-normed hidden states of the k soft rows
-                        (the "pooled final hidden state" of the Fig. 2 caption) */
+                        (the pooled read-out the Fig. 2 caption names) */
 } sp_pool;
 
 enum {

@@ -23,8 +23,8 @@ values (bf16 and fp32 inputs convert to fp64 without rounding):
   6. a_j = x_j + W_o concat_h(o_{j,h});
   7. y_j = a_j + W_down(silu(W_gate w_j) * (W_up w_j)), w_j = RMSNorm(a_j; gamma_post);
   8. f_j = RMSNorm(y_j; gamma_final); pooled = f_{k-1} ("last", the read-out of
-     the k-th step, Sec. 3.2) or the mean of f_0..f_{k-1} ("mean", the "pooled
-     final hidden state" of the Fig. 2 caption);
+     the k-th step, Sec. 3.2) or the mean of f_0..f_{k-1} ("mean", the pooled
+     read-out the Fig. 2 caption names);
   9. logits = W_cls pooled (+ b_cls): the linear head of Sec. 3.2 with C rows
      instead of one, returned before any sigmoid.
 
@@ -203,7 +203,7 @@ def probe_batch(kv_list, soft_prompt, weights: dict, shape: HeadShape, taps: boo
 #   * w_fc is stored [d][2d]; its columns 0..d-1 multiply the normed hidden
 #     state and columns d..2d-1 the normed soft-prompt vector (the order in
 #     which Sec. 3.1 lists the two inputs);
-#   * the "output hidden state" a step hands on (and the one the classifier
+#   * the output hidden state a step hands on (and the one the classifier
 #     reads) is the final-normed f_t;
 #   * step t (0-based) sits at position N + t and attends to the N cached keys
 #     plus the soft keys of steps 0..t (its own included);
