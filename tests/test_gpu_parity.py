@@ -274,3 +274,45 @@ def test_full_size_sampled_sequences(w, dev):
     probe.close()
     del kv, params
     torch.cuda.empty_cache()
+
+
+def test_debug_mode_reports_invalid_device_data(dev):
+    """SP_FLAG_DEBUG: a seq_len past max_seq_len, a negative one, or a block id past
+    the pool makes the forward (one-pass, multi-task or recursive) skip its work and
+    sp_probe_check_device_error report SP_ERR_DEVICE_DATA; valid data then runs clean
+    and matches the oracle."""
+    w = configs.SMALL_BF16
+    kv, params, kv_d, p_d = small_case(w, dev)
+    fusion = {k: v.to(dev) for k, v in inputs.fusion_params(w, "cpu").items()}
+    tasks = {k: (None if v is None else v.to(dev)) for k, v in inputs.task_params(w, 2, "cpu").items()}
+    probe = binding.Probe(w, flags=binding.SP_FLAG_DEBUG, max_tasks=2)
+    good_lens = kv_d.seq_lens.clone()
+    good_table = kv_d.block_table.clone()
+    bad_cases = []
+    lens = good_lens.clone(); lens[2] = w.max_seq_len() + 1; bad_cases.append(("long seq_len", lens, good_table))
+    lens = good_lens.clone(); lens[0] = -3; bad_cases.append(("negative seq_len", lens, good_table))
+    table = good_table.clone(); table[4, 0] = kv_d.num_blocks + 7; bad_cases.append(("block id", good_lens, table))
+    runs = {
+        "one-pass": lambda kvx, out: probe.forward(kvx, p_d, out),
+        "recursive": lambda kvx, out: probe.forward_recursive(kvx, p_d, fusion, out),
+        "tasks": None,
+    }
+    for what, lens, table in bad_cases:
+        for name, run in runs.items():
+            kvx = inputs.KVCache(kv_d.pool, table, lens, kv_d.block_size, kv_d.max_blocks_per_seq, kv_d.n_kv,
+                                 kv_d.head_dim)
+            out = torch.full((w.batch, w.n_classes), 5.0, device=dev)
+            if name == "tasks":
+                out2 = torch.full((w.batch, 2, w.n_classes), 5.0, device=dev)
+                probe.forward_multi(kvx, p_d, tasks["soft_prompts"], tasks["w_cls"], tasks["b_cls"], out2)
+                assert probe.check_device_error() == -7, (what, name)
+                assert torch.all(out2 == 5.0), (what, name)
+            else:
+                run(kvx, out)
+                assert probe.check_device_error() == -7, (what, name)
+                assert torch.all(out == 5.0), (what, name)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    assert probe.check_device_error() == 0
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, "after the errors")
+    probe.close()
