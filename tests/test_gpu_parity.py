@@ -316,3 +316,35 @@ def test_debug_mode_reports_invalid_device_data(dev):
     ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
     H.check_logits(got, ref, w.dtype, "after the errors")
     probe.close()
+
+
+def test_largest_hidden_width(dev):
+    """hidden = 16384, the widest the row kernels take (RMSNorm, RoPE scatter,
+    classifier), against the oracle."""
+    w = configs.Workload(name="wide_bf16", dtype="bf16", batch=2, k=2, hidden=16384, n_q_heads=4,
+                         n_kv_heads=2, head_dim=64, intermediate=64, n_classes=2,
+                         seq_len=("list", (40, 3)), seed=97)
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, "one-pass")
+    probe.close()
+
+
+def test_many_tasks(dev):
+    """Sixteen tasks of four soft rows in one call (64 soft rows, 256 query rows
+    per KV head over several query groups), every task against the oracle."""
+    from oracle import probe as oracle
+    w = configs.SMALL_BF16.replace(name="small_16_tasks", seed=98)
+    T = 16
+    kv, params, kv_d, p_d = small_case(w, dev)
+    tasks = inputs.task_params(w, T, "cpu")
+    probe = binding.Probe(w, max_tasks=T)
+    got = probe.forward_multi(kv_d, p_d, tasks["soft_prompts"].to(dev), tasks["w_cls"].to(dev)).cpu().numpy()
+    probe.close()
+    kvs = [tuple(t.double().numpy() for t in kv.logical_kv(b)) for b in range(w.batch)]
+    ref = oracle.probe_batch_tasks(kvs, tasks["soft_prompts"].double().numpy(), tasks["w_cls"].double().numpy(),
+                                   None, H.oracle_weights(params), H.head_shape(w))
+    for t in range(T):
+        H.check_logits(got[:, t], ref[:, t], w.dtype, f"task {t}")
