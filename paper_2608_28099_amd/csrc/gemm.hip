@@ -283,12 +283,18 @@ hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
 }
 
 // Tile shapes, in order of preference (measured on the probe's projection
-// shapes): (BM, BN, waves along M, waves along N, stages, K-step depth).
+// shapes, 512 to 8192 rows): (BM, BN, waves along M, waves along N, K-step
+// depth); the stage counts are in launch_gemm.  SwiGLU (gate/up) prefers the
+// widest tiles; the residual epilogues (o, down) prefer 256 x 128 tiles with
+// 64-deep steps, which at 2048-8192 rows take half the time of 128 x 64.
 struct TileShape { int bm, bn, wgm, wgn, bk; };
-constexpr int kNumTiles = 7;
-constexpr TileShape kTiles[kNumTiles] = {{256, 192, 4, 2, 32}, {128, 64, 4, 2, 64}, {64, 64, 2, 2, 64},
-                                         {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64}, {16, 16, 1, 1, 64},
-                                         {16, 32, 1, 1, 32}};
+constexpr int kNumTiles = 9;
+constexpr TileShape kTiles[kNumTiles] = {
+    {256, 256, 4, 2, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
+    {64, 64, 2, 2, 64},   {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64},  {16, 16, 1, 1, 64},
+    {16, 32, 1, 1, 32}};
+constexpr int kOrderSwiglu[kNumTiles] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
+constexpr int kOrderResid[kNumTiles] = {2, 1, 0, 3, 4, 5, 6, 7, 8};
 
 bool tile_ok(const GemmParams& p, Epilogue epi, const TileShape& t) {
   if (p.N % t.bn || p.K % t.bk) return false;
@@ -336,22 +342,26 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     return launch_split<256, 128, 4, 2, 3, 64>(epi, p, 4, s);
   // First tile (in preference order) that gives at least one workgroup per
   // compute unit (256), else the valid tile with the most workgroups.
+  const int* order = epi == kEpiSwiglu ? kOrderSwiglu : kOrderResid;
   int best = -1;
   long best_tiles = -1;
-  for (int c = 0; c < kNumTiles; ++c) {
+  for (int i = 0; i < kNumTiles; ++i) {
+    const int c = order[i];
     if (!tile_ok(p, epi, kTiles[c])) continue;
     const long tiles = (long)((p.M + kTiles[c].bm - 1) / kTiles[c].bm) * (p.N / kTiles[c].bn);
     if (tiles >= 256) { best = c; break; }
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
   switch (best) {
-    case 0: return launch_lds_tile<256, 192, 4, 2, 3, 32>(epi, p, s);
-    case 1: return launch_lds_tile<128, 64, 4, 2, 6, 64>(epi, p, s);
-    case 2: return launch_lds_tile<64, 64, 2, 2, 8, 64>(epi, p, s);
-    case 3: return launch_lds_tile<32, 64, 1, 2, 8, 64>(epi, p, s);
-    case 4: return launch_lds_tile<16, 32, 1, 1, 8, 64>(epi, p, s);
-    case 5: return launch_lds_tile<16, 16, 1, 1, 8, 64>(epi, p, s);
-    case 6: return launch_lds_tile<16, 32, 1, 1, 8, 32>(epi, p, s);
+    case 0: return launch_lds_tile<256, 256, 4, 2, 3, 32>(epi, p, s);
+    case 1: return launch_lds_tile<256, 192, 4, 2, 3, 32>(epi, p, s);
+    case 2: return launch_lds_tile<256, 128, 4, 2, 3, 64>(epi, p, s);
+    case 3: return launch_lds_tile<128, 64, 4, 2, 6, 64>(epi, p, s);
+    case 4: return launch_lds_tile<64, 64, 2, 2, 8, 64>(epi, p, s);
+    case 5: return launch_lds_tile<32, 64, 1, 2, 8, 64>(epi, p, s);
+    case 6: return launch_lds_tile<16, 32, 1, 1, 8, 64>(epi, p, s);
+    case 7: return launch_lds_tile<16, 16, 1, 1, 8, 64>(epi, p, s);
+    case 8: return launch_lds_tile<16, 32, 1, 1, 8, 32>(epi, p, s);
   }
   return hipErrorInvalidValue;
 }
