@@ -128,6 +128,32 @@ def test_head_dims_and_splits(hd, dev):
         probe.close()
 
 
+@pytest.mark.parametrize("case", [
+    # (query heads, KV heads, lengths, splits): 64 rows per KV head (4 waves per
+    # workgroup) with 3, 6 and 4 splits; 80 rows (5 waves) with 4 splits
+    (16, 4, (700, 256, 1, 0, 513, 768), 3),
+    (16, 4, (1500, 700, 1, 1290, 33), 6),
+    (16, 4, (1000, 257, 31, 769), 4),
+    (10, 2, (1024, 3, 600, 255), 4),
+], ids=["g4_s3", "g4_s6", "g4_s4", "g5_s4"])
+def test_multi_split_wide_query_tiles(case, dev):
+    """Several splits per sequence with 4- and 5-wave workgroups: ragged tails
+    in any split, splits with no tokens, empty sequences."""
+    n_q, n_kv, lens, n_splits = case
+    w = configs.Workload(name=f"splits_g{n_q // n_kv}_{n_splits}", dtype="bf16", batch=len(lens), k=16,
+                         hidden=256, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=128,
+                         intermediate=320, n_classes=3, seq_len=("list", lens), kv_std=1.0,
+                         weight_std=0.05, seed=41)
+    announce(f"[multi-split] {w.name} lens={lens}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w, split_len=256)
+    assert probe.plan(w.batch)["max_splits"] == n_splits
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, w.name)
+    probe.close()
+
+
 def test_projection_tile_shapes(dev):
     """Shapes whose projections select the fallback tiles of the bf16 GEMM:
     64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, the
