@@ -266,8 +266,15 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   __builtin_assume(tid < 64 * W);
   __builtin_assume(wave >= 0 && wave < W);
-  const int s = blockIdx.x;
-  const int g = blockIdx.y / p.n_qgroups, qg = blockIdx.y % p.n_qgroups;
+  // Grid (KV head + n_kv * query group, split, sequence): workgroups are dealt
+  // to the 8 XCDs round-robin in linear order, so with n_kv a multiple of 8
+  // each XCD takes whole KV heads (the same work for every head), and the
+  // query groups of one (sequence, KV head, split), which read the same K/V,
+  // run on one XCD at about the same time.  With the split index fastest,
+  // the splits past the end of short sequences (which exit at once) would all
+  // fall on the same XCDs.
+  const int s = blockIdx.y;
+  const int g = blockIdx.x % p.n_kv, qg = blockIdx.x / p.n_kv;
   const int b = blockIdx.z;
   if (p.err && *p.err) return;
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
@@ -680,7 +687,7 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
 
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
   if (p.bs_log2 < 4 || p.split_len % 32) return hipErrorInvalidValue;
-  const dim3 grid(p.max_splits, p.n_kv * p.n_qgroups, batch);
+  const dim3 grid(p.n_kv * p.n_qgroups, p.max_splits, batch);
 #define SP_ATTN_CASE(HD_, W_)                                                          \
   if (hd == HD_ && waves == W_) {                                                      \
     hipLaunchKernelGGL((attn_split_bf16<HD_, W_>), grid, dim3(64 * W_), 0, s, p);       \

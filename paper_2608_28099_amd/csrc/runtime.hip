@@ -110,17 +110,16 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows) {
     a.split_len = c.split_len;
   } else if (c.dtype == SP_BF16) {
     // Splits sized so that the attention grid at the full batch and length is
-    // about one round of resident workgroups (256 compute units x 3 workgroups
-    // of <= 4 waves, x 2 above): every round of workgroups costs a start-up
-    // and a drain.  At most max_seq_len / 2 (two splits for the longest
-    // sequence, so batches of mixed lengths still balance), at least 1024,
-    // a multiple of 256.
+    // at least one round of resident workgroups (256 compute units x 3
+    // workgroups of <= 4 waves, x 2 above), and at most a third of the longest
+    // sequence: three splits for the longest sequences measured faster than
+    // one, two or four on uniform and ragged batches alike, whether the grid
+    // is one round or many.  At least 1024 tokens, a multiple of 256.
     const int64_t slots = 256 * (a.waves <= 4 ? 3 : 2);
     const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * a.n_qgroups;
     const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
-    const int64_t half = ((int64_t)c.max_seq_len / 2 + 255) / 256 * 256;
-    int64_t sl = (want + 255) / 256 * 256;
-    sl = std::min(sl, half);
+    const int64_t third = ((int64_t)c.max_seq_len + 2) / 3;
+    const int64_t sl = (std::min(want, third) + 255) / 256 * 256;
     a.split_len = (int)std::max<int64_t>(sl, 1024);
   } else {
     // fp32 path: at most 8 splits per sequence, between 1024 and 16384 tokens each
