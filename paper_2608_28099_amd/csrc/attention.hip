@@ -694,7 +694,8 @@ hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int bat
     return hipGetLastError();                                                          \
   }
   SP_ATTN_CASE(128, 1) SP_ATTN_CASE(128, 2) SP_ATTN_CASE(128, 3) SP_ATTN_CASE(128, 4)
-  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8)
+  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
+  SP_ATTN_CASE(128, 12)
   SP_ATTN_CASE(64, 1) SP_ATTN_CASE(64, 2) SP_ATTN_CASE(64, 3) SP_ATTN_CASE(64, 4)
   SP_ATTN_CASE(64, 5) SP_ATTN_CASE(64, 6) SP_ATTN_CASE(64, 8) SP_ATTN_CASE(64, 10)
   SP_ATTN_CASE(64, 12) SP_ATTN_CASE(64, 16)

@@ -67,7 +67,7 @@ struct AttnParams {
 };
 // Cache tokens only (the soft keys are folded in by the merge).
 // bf16-storage path (bf16 MFMA, split Q and P): head_dim 64/128, `waves` 16-row
-// query tiles per workgroup (1, 2, 3, 4, 5, 6 or 8; up to 16 for head_dim 64).
+// query tiles per workgroup (1, 2, 3, 4, 5, 6, 8, 10 or 12; up to 16 for head_dim 64).
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s);
 // fp32 VALU path: head_dim 64/128, rows <= 64.
 hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);

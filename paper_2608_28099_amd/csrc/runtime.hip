@@ -92,11 +92,13 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows) {
     a.n_qgroups = 1;
     a.r_alloc = rows;
   } else {
-    // one wave per 16-row query tile, at most 8 (head_dim 128) or 16 (64) waves
-    // per workgroup, whose register budget then still fits without spills; the
-    // sizes below are the instantiated ones (extra tiles are padding)
+    // one wave per 16-row query tile, at most 12 (head_dim 128: a compute unit
+    // holds 12 waves of its ~150 VGPRs) or 16 (64) waves per workgroup, so one
+    // workgroup reads each K/V tile for as many rows as fit (the 160 rows of
+    // the 27B shape as one group of ten: 28% faster than two groups of five);
+    // the sizes below are the instantiated ones (extra tiles are padding)
     static const int kWaves[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
-    const int max_w = c.head_dim == 128 ? 8 : 16;
+    const int max_w = c.head_dim == 128 ? 12 : 16;
     const int groups = (tiles + max_w - 1) / max_w;
     const int per_group = (tiles + groups - 1) / groups;
     int w = max_w;
@@ -110,12 +112,14 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows) {
     a.split_len = c.split_len;
   } else if (c.dtype == SP_BF16) {
     // Splits sized so that the attention grid at the full batch and length is
-    // at least one round of resident workgroups (256 compute units x 3
-    // workgroups of <= 4 waves, x 2 above), and at most a third of the longest
+    // at least one round of resident workgroups, and at most a third of the longest
     // sequence: three splits for the longest sequences measured faster than
     // one, two or four on uniform and ragged batches alike, whether the grid
     // is one round or many.  At least 1024 tokens, a multiple of 256.
-    const int64_t slots = 256 * (a.waves <= 4 ? 3 : 2);
+    // workgroups per compute unit: 3 by LDS, and at most 12 waves (head_dim
+    // 128) or 20 (64) by VGPRs
+    const int64_t per_cu = std::min(3, (c.head_dim == 128 ? 12 : 20) / a.waves);
+    const int64_t slots = 256 * std::max<int64_t>(per_cu, 1);
     const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * a.n_qgroups;
     const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
     const int64_t third = ((int64_t)c.max_seq_len + 2) / 3;

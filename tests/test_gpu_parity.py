@@ -129,25 +129,30 @@ def test_head_dims_and_splits(hd, dev):
 
 
 @pytest.mark.parametrize("case", [
-    # (query heads, KV heads, lengths, splits): 64 rows per KV head (4 waves per
-    # workgroup) with 3, 6 and 4 splits; 80 rows (5 waves) with 4 splits
-    (16, 4, (700, 256, 1, 0, 513, 768), 3),
-    (16, 4, (1500, 700, 1, 1290, 33), 6),
-    (16, 4, (1000, 257, 31, 769), 4),
-    (10, 2, (1024, 3, 600, 255), 4),
-], ids=["g4_s3", "g4_s6", "g4_s4", "g5_s4"])
+    # (query heads, KV heads, k, lengths, splits): 64 rows per KV head (4 waves
+    # per workgroup) with 3, 6 and 4 splits; 80 rows (5 waves) with 4 splits;
+    # 160 rows (one workgroup of 10 waves) and 192 rows (12 waves)
+    (16, 4, 16, (700, 256, 1, 0, 513, 768), 3),
+    (16, 4, 16, (1500, 700, 1, 1290, 33), 6),
+    (16, 4, 16, (1000, 257, 31, 769), 4),
+    (10, 2, 16, (1024, 3, 600, 255), 4),
+    (10, 2, 32, (700, 0, 33, 512), 3),
+    (8, 2, 48, (300, 769, 17), 4),
+], ids=["g4_s3", "g4_s6", "g4_s4", "g5_s4", "w10_s3", "w12_s4"])
 def test_multi_split_wide_query_tiles(case, dev):
-    """Several splits per sequence with 4- and 5-wave workgroups: ragged tails
+    """Several splits per sequence with 4- to 12-wave workgroups: ragged tails
     in any split, splits with no tokens, empty sequences."""
-    n_q, n_kv, lens, n_splits = case
-    w = configs.Workload(name=f"splits_g{n_q // n_kv}_{n_splits}", dtype="bf16", batch=len(lens), k=16,
+    n_q, n_kv, k, lens, n_splits = case
+    w = configs.Workload(name=f"splits_g{n_q // n_kv}_k{k}_{n_splits}", dtype="bf16", batch=len(lens), k=k,
                          hidden=256, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=128,
                          intermediate=320, n_classes=3, seq_len=("list", lens), kv_std=1.0,
                          weight_std=0.05, seed=41)
     announce(f"[multi-split] {w.name} lens={lens}")
     kv, params, kv_d, p_d = small_case(w, dev)
     probe = binding.Probe(w, split_len=256)
-    assert probe.plan(w.batch)["max_splits"] == n_splits
+    plan = probe.plan(w.batch)
+    assert plan["max_splits"] == n_splits
+    assert plan["query_groups"] == 1 and plan["rows_per_kv_head"] == k * n_q // n_kv
     got = probe.forward(kv_d, p_d).cpu().numpy()
     ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
     H.check_logits(got, ref, w.dtype, w.name)
