@@ -166,8 +166,9 @@ def cpu_baseline(w, kv, params, seconds: float, fusion=None, tasks=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the forward is per-sequence "
-              "independent and shards by sequence, which this build does not run.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the forward is independent "
+              "per sequence and would shard by sequence, but only the one-GPU path exists.",
+              file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -8,7 +8,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libsp_probe.so")
-SOURCES = ["attention.hip", "gemm.hip", "rowops.hip", "runtime.hip"]
+SOURCES = ["attention.hip", "merge.hip", "gemm.hip", "rowops.hip", "runtime.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -6,6 +6,13 @@
 
 namespace sp {
 
+// Context length of sequence b, clamped to [0, max_seq_len].
+__device__ __forceinline__ int clamp_len(const int* seq_lens, int b, int max_seq_len) {
+  int n = seq_lens[b];
+  return n < 0 ? 0 : (n > max_seq_len ? max_seq_len : n);
+}
+
+
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
