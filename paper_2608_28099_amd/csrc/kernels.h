@@ -92,6 +92,7 @@ struct MergeParams {
   // its output goes to row b * out_rows + out_off + qi.
   int k_task, q_first, q_per_task, step, out_rows, out_off;
   int per_seq;             // v_soft is [B][n_kv][ks][hd] instead of [n_kv][ks][hd]
+  int rw;                  // soft rows per workgroup (set by launch_merge)
 };
 // dt: storage dtype of the config (the output is fp16 for bf16 storage)
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s);

@@ -159,6 +159,22 @@ def test_multi_split_wide_query_tiles(case, dev):
     probe.close()
 
 
+def test_merge_rows_per_workgroup(dev):
+    """A batch large enough that the merge gives each workgroup several soft
+    rows (256 sequences x 8 KV heads, k = 48: blocks of 32 soft rows, the second
+    block of each sequence partial), ragged and empty contexts."""
+    w = configs.Workload(name="merge_blocks", dtype="bf16", batch=256, k=48, hidden=256, n_q_heads=16,
+                         n_kv_heads=8, head_dim=128, intermediate=128, n_classes=3,
+                         seq_len=("uniform", 0, 40), kv_std=1.0, weight_std=0.05, seed=42)
+    announce(f"[merge blocks] {w.name}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    H.check_logits(got, ref, w.dtype, w.name)
+    probe.close()
+
+
 def test_projection_tile_shapes(dev):
     """Shapes whose projections select the fallback tiles of the bf16 GEMM:
     64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, the

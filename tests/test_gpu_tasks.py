@@ -60,6 +60,11 @@ TASK_CASES = [
     (configs.SMALL_BF16, 3, binding.SP_FLAG_LAST_ROW_ONLY),
     (configs.SMALL_BF16.replace(name="small_bf16_k17", k=17, seed=80), 2, binding.SP_FLAG_LAST_ROW_ONLY),
     (configs.TINY_RAGGED_F32, 2, binding.SP_FLAG_LAST_ROW_ONLY),
+    # 64 sequences x 8 KV heads x 2 tasks of k = 48: the merge takes blocks of 32
+    # soft rows (two per task, the second partial); 384 query rows per KV head
+    (configs.Workload(name="tasks_merge_blocks", dtype="bf16", batch=64, k=48, hidden=256, n_q_heads=32,
+                      n_kv_heads=8, head_dim=128, intermediate=128, n_classes=2,
+                      seq_len=("uniform", 1, 64), kv_std=1.0, weight_std=0.05, seed=43), 2, 0),
 ]
 
 
