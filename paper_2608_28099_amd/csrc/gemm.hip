@@ -340,6 +340,19 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
   if (p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kLongK) && p.part &&
       (size_t)4 * p.M * p.N * sizeof(float) <= p.part_bytes)
     return launch_split<256, 128, 4, 2, 3, 64>(epi, p, 4, s);
+  // 33..256 rows, epilogues other than SwiGLU (o, down, the fusion products):
+  // the weights stream with few tiles, so 128 x 64 tiles with K split until
+  // the grid has 256 workgroups (9B-shaped down on 128 rows: 48 us against 70;
+  // o on 256 rows of the 27B shape: 58 us against 71).  SwiGLU keeps its wide
+  // tiles, which measured faster there.
+  constexpr TileShape kMid{128, 64, 4, 2, 64};
+  if (epi != kEpiSwiglu && p.M > 32 && p.M <= 256 && tile_ok(p, epi, kMid) && p.part) {
+    const long tiles = (long)((p.M + 127) / 128) * (p.N / 64);
+    int ks = 2;
+    while (ks < 8 && tiles * ks < 256) ks *= 2;
+    if (p.K / 64 / ks >= 8 && (size_t)ks * p.M * p.N * sizeof(float) <= p.part_bytes)
+      return launch_split<128, 64, 4, 2, 6, 64>(epi, p, ks, s);
+  }
   // First tile (in preference order) that gives at least one workgroup per
   // compute unit (256), else the valid tile with the most workgroups.
   const int* order = epi == kEpiSwiglu ? kOrderSwiglu : kOrderResid;
