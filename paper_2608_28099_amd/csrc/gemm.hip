@@ -9,9 +9,10 @@
 // step); weights stay bf16 in LDS and are converted exactly to fp16 (|w| in
 // [2^-14, 65504]) as a wave reads its fragments.  A row of a stage tile is BK
 // values = PPR 16-byte pieces; piece kp of row r sits at
-//   r * PPR + (kp ^ ((r >> (4 - log2 PPR)) & (PPR - 1)))
-// so the 16 lanes that read piece kp of 16 consecutive rows hit 16 distinct
-// 16-byte bank groups.
+//   r * PPR + (kp ^ ((r >> 1) & (PPR - 1)))
+// which leaves the 16-byte fragment reads of 16 consecutive rows free of LDS
+// bank conflicts for both PPR = 4 and 8 (the LDS bank-conflict counter reads 0;
+// a shift of 2 for PPR = 4 measured conflicts on half the LDS cycles).
 // SwiGLU: the BN weight rows of a tile alternate 16 gate rows and the 16
 // matching up rows, so every lane holds gate and up of the same outputs.
 // Split-K (PART, small M: the product then streams the weights with too few
@@ -31,7 +32,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   constexpr int NW = WGM * WGN, WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
   constexpr int PPR = BK / 8;                        // 16-byte pieces per tile row
   constexpr int RPI = 64 / PPR;                      // tile rows per 64-piece load
-  constexpr int SWS = PPR == 4 ? 2 : 1;              // swizzle: kp ^ ((r >> SWS) & (PPR - 1))
+  constexpr int SWS = 1;                             // swizzle: kp ^ ((r >> SWS) & (PPR - 1))
   constexpr int NIA = BM / RPI, NI = NIA + BN / RPI;  // 64-piece loads per step
   constexpr int IPW = (NI + NW - 1) / NW;            // loads per wave per step
   constexpr int STAGE = (BM + BN) * PPR;             // pieces per stage
