@@ -22,9 +22,11 @@
  *  - All calls return sp_status and never abort or throw.  Checks that can be
  *    made on the host run before anything is enqueued: on error no work is
  *    queued and the outputs are untouched.
- *  - sp_probe_forward enqueues work on `stream` (a hipStream_t; NULL = the
- *    null stream) and returns without waiting; it allocates nothing and never
- *    synchronises the host unless a debug/profiling call below says so.
+ *  - sp_probe_forward (and _multi, _recursive) enqueues work on `stream` (a
+ *    hipStream_t; NULL = the null stream) and returns without waiting; it
+ *    allocates nothing, records no memset and never synchronises the host
+ *    unless a debug/profiling call below says so, so a call can be captured
+ *    into a HIP graph and replayed (without SP_FLAG_PROFILE / SP_FLAG_DEBUG).
  *  - One handle carries one workspace: forwards on the same handle must be
  *    ordered (same stream, or caller-synchronised).  Distinct handles are
  *    independent.
