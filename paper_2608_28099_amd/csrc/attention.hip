@@ -304,9 +304,19 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     const int* bt_row = p.block_table ? p.block_table + (int64_t)b * p.mbps + lb0 : nullptr;
     if (bt_row)
       for (int i = tid; i < min(nlb, 2 * kIdWin); i += 64 * W) blk_ids[i / kIdWin][i % kIdWin] = bt_row[i];
-    auto phys = [&](int rel) __attribute__((always_inline)) -> int64_t {
-      return bt_row ? (int64_t)__builtin_amdgcn_readfirstlane(blk_ids[(rel / kIdWin) & 1][rel % kIdWin])
-                    : (int64_t)b * p.mbps + lb0 + rel;
+    // Physical blocks of logical blocks lb0 + ra and lb0 + rb; both table reads
+    // are issued before either is used (one LDS round trip, not two).
+    auto phys2 = [&](int ra, int rb, int64_t& pa, int64_t& pb) __attribute__((always_inline)) {
+      if (bt_row) {
+        const unsigned ua = (unsigned)ra, ub = (unsigned)rb;
+        const int ia = blk_ids[(ua / kIdWin) & 1][ua % kIdWin];
+        const int ib = blk_ids[(ub / kIdWin) & 1][ub % kIdWin];
+        pa = (int64_t)__builtin_amdgcn_readfirstlane(ia);
+        pb = (int64_t)__builtin_amdgcn_readfirstlane(ib);
+      } else {
+        pa = (int64_t)b * p.mbps + lb0 + ra;
+        pb = (int64_t)b * p.mbps + lb0 + rb;
+      }
     };
     auto load_window = [&](int w) __attribute__((always_inline)) {
       for (int j = wave; j < kIdWin / 64; j += W) {
@@ -346,7 +356,8 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     auto issue = [&](int u, int buf) __attribute__((always_inline)) {
       const int ta = t0 + 32 * u;
       const int tb = ta + 16 < t1 ? ta + 16 : ta;
-      const int64_t ba = phys((ta >> p.bs_log2) - lb0), bb = phys((tb >> p.bs_log2) - lb0);
+      int64_t ba, bb;
+      phys2((ta >> p.bs_log2) - lb0, (tb >> p.bs_log2) - lb0, ba, bb);
       const int sa = ta & (bs - 1), sbb = tb & (bs - 1);
       const bf16* g0 = kbase + ba * p.k_sb + sa * 8;
       const bf16* g1 = kbase + bb * p.k_sb + sbb * 8;
