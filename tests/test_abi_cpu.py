@@ -124,3 +124,15 @@ def test_workspace_grows_with_tasks():
     four = binding.sp_probe_workspace_bytes(binding.make_config(w, max_tasks=4))
     pruned = binding.sp_probe_workspace_bytes(binding.make_config(w, max_tasks=4, flags=binding.SP_FLAG_LAST_ROW_ONLY))
     assert four > 3 * one // 2 and 0 < pruned
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU; --gpus N > 1 exits with status 2 and says why,
+    before anything touches a device."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    res = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr and not res.stdout.strip()
