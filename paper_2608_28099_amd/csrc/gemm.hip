@@ -287,11 +287,13 @@ hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
 // shapes, 512 to 8192 rows): (BM, BN, waves along M, waves along N, K-step
 // depth); the stage counts are in launch_gemm.  SwiGLU (gate/up) prefers the
 // widest tiles; the residual epilogues (o, down) prefer 256 x 128 tiles with
-// 64-deep steps, which at 2048-8192 rows take half the time of 128 x 64.
+// 64-deep steps, which at 2048-8192 rows take half the time of 128 x 64.  The
+// 256 x 256 tile runs 2 x 4 waves: each weight fragment is then converted by
+// two waves instead of four (gate/up on 8192 rows 9% faster than 4 x 2).
 struct TileShape { int bm, bn, wgm, wgn, bk; };
 constexpr int kNumTiles = 9;
 constexpr TileShape kTiles[kNumTiles] = {
-    {256, 256, 4, 2, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
+    {256, 256, 2, 4, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
     {64, 64, 2, 2, 64},   {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64},  {16, 16, 1, 1, 64},
     {16, 32, 1, 1, 32}};
 constexpr int kOrderSwiglu[kNumTiles] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
@@ -367,7 +369,7 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
   switch (best) {
-    case 0: return launch_lds_tile<256, 256, 4, 2, 3, 32>(epi, p, s);
+    case 0: return launch_lds_tile<256, 256, 2, 4, 3, 32>(epi, p, s);
     case 1: return launch_lds_tile<256, 192, 4, 2, 3, 32>(epi, p, s);
     case 2: return launch_lds_tile<256, 128, 4, 2, 3, 64>(epi, p, s);
     case 3: return launch_lds_tile<128, 64, 4, 2, 6, 64>(epi, p, s);
