@@ -170,3 +170,44 @@ def test_tasks_full_size_sampled_sequences(w, T, flags, dev):
     probe.close()
     del kv, params
     torch.cuda.empty_cache()
+
+
+LIMIT_CASES = [
+    # k = 64 soft rows (the largest k) x 16 tasks = 1024 rows per sequence (the
+    # largest tasks x k), 64 classes (the largest classifier), one query head per
+    # KV head, an empty context next to a ragged one
+    (configs.Workload(name="limit_k64_t16_c64", dtype="bf16", batch=2, k=64, hidden=256, n_q_heads=2,
+                      n_kv_heads=2, head_dim=128, intermediate=128, n_classes=64,
+                      seq_len=("list", (0, 333)), kv_std=1.0, weight_std=0.05, seed=61), 16, 0),
+    # 64 tasks (the largest task count) of k = 16 with four query heads per KV
+    # head: 4096 query rows per KV head in one call, head_dim 64
+    (configs.Workload(name="limit_t64_g4_hd64", dtype="bf16", batch=2, k=16, hidden=256, n_q_heads=8,
+                      n_kv_heads=2, head_dim=64, intermediate=128, n_classes=2,
+                      seq_len=("list", (257, 40)), kv_std=1.0, weight_std=0.05, seed=62), 64, 0),
+    # the same 64 tasks with only each task's last row past the attention
+    (configs.Workload(name="limit_t64_last", dtype="bf16", batch=2, k=16, hidden=256, n_q_heads=8,
+                      n_kv_heads=2, head_dim=64, intermediate=128, n_classes=2,
+                      seq_len=("list", (257, 40)), kv_std=1.0, weight_std=0.05, seed=63), 64,
+     binding.SP_FLAG_LAST_ROW_ONLY),
+    # the fp32 path at its cap of 64 query rows per KV head (4 tasks x k 8 x 2)
+    (configs.Workload(name="limit_f32_rows64", dtype="f32", batch=3, k=8, hidden=128, n_q_heads=4,
+                      n_kv_heads=2, head_dim=64, intermediate=64, n_classes=3,
+                      seq_len=("list", (1, 64, 190)), kv_std=1.0, weight_std=0.1, seed=64), 4, 0),
+]
+
+
+@pytest.mark.parametrize("w,T,flags", LIMIT_CASES, ids=lambda x: getattr(x, "name", str(x)))
+def test_largest_row_counts(w, T, flags, dev):
+    """The largest k, task count, tasks x k, class count and fp32 row count the
+    library accepts, every task against the oracle."""
+    announce(f"[limits] {w.name} T={T} flags={flags}")
+    kv, params, tasks, kv_d, p_d, t_d = case(w, dev, T)
+    probe = binding.Probe(w, flags=flags, max_tasks=T)
+    try:
+        got = run_tasks(probe, kv_d, p_d, t_d, T).cpu().numpy()
+        ref = oracle_tasks(w, kv, params, tasks)
+        assert got.shape == (w.batch, T, w.n_classes)
+        err = max(H.check_logits(got[:, t], ref[:, t], w.dtype, f"{w.name} task {t}") for t in range(T))
+        announce(f"[limits] {w.name}: max err {err:.3e}")
+    finally:
+        probe.close()
