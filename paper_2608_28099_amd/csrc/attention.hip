@@ -245,7 +245,7 @@ __device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, 
 
 // W waves per workgroup, one per 16-row query tile.  Three LDS stages: unit u
 // is computed from stage u % 3 while units u + 1 and u + 2 are in flight.
-template <int HD, int W>
+template <int HD, int W, bool ROT>
 __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   constexpr int NC = HD / 32, NT = HD / 16;
   constexpr int NI = UnitLayout<HD>::NI;
@@ -384,6 +384,23 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     int buf = 0;
     // One unit: wait for its loads, publish them, issue unit u + 2, compute.
     // The first unit is peeled (raw scores; see qk_unit).
+    // Co-resident workgroups share a compute unit's wave arbiter, which favours
+    // the oldest waves: in a grid of one round (every workgroup resident from
+    // the start), the workgroups of a compute unit would end one after another
+    // in dispatch order and the launch on a tail at one or two per compute
+    // unit.  There (ROT) their wave priorities rotate with the 100 MHz
+    // real-time counter (every 2^12 ticks, 41 us): a workgroup's dispatch pass
+    // (256 compute units per pass) sets its phase, so the workgroups of one
+    // compute unit take turns at each priority level.  Timing only: what each
+    // workgroup computes does not change.
+    const int rot_phase = (int)(((blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z)) >> 8) % 3);
+    auto rotate_priority = [&]() __attribute__((always_inline)) {
+      const int ep = (int)((__builtin_amdgcn_s_memrealtime() >> 12) % 3);
+      const int pr = __builtin_amdgcn_readfirstlane((rot_phase + ep) % 3);
+      if (pr == 0) __builtin_amdgcn_s_setprio(0);
+      else if (pr == 1) __builtin_amdgcn_s_setprio(1);
+      else __builtin_amdgcn_s_setprio(2);
+    };
     auto step = [&](int u, auto first) __attribute__((always_inline)) {
       // this wave's loads of unit u are done once at most those of unit u + 1 remain
       if (u < last)
@@ -392,6 +409,8 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
         wait_vmcnt<0>();
       // every wave's loads of unit u have landed and every wave is done with unit u - 1
       lds_barrier();
+      if constexpr (ROT)
+        if ((u & 3) == 0) rotate_priority();
       const int limit = t1 - (t0 + 32 * u);
       if (limit < 32) {
         zero_tail<HD, W>(stage[buf], limit, tid);
@@ -526,17 +545,32 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
   if (p.bs_log2 < 4 || p.split_len % 32) return hipErrorInvalidValue;
   const dim3 grid(p.n_kv * p.n_qgroups, p.max_splits, batch);
-#define SP_ATTN_CASE(HD_, W_)                                                          \
-  if (hd == HD_ && waves == W_) {                                                      \
-    hipLaunchKernelGGL((attn_split_bf16<HD_, W_>), grid, dim3(64 * W_), 0, s, p);       \
-    return hipGetLastError();                                                          \
+  // Rotating priorities pays where several multi-wave workgroups share each
+  // compute unit for the whole launch: a grid of at most one round (long
+  // uniform batches: 83% of HBM peak against 78%).  Grids of many rounds
+  // refill compute units as workgroups end, and one-wave workgroups do not
+  // stagger; there the clock reads only cost time (2-5% measured).
+  const int per_cu = attn_wgs_per_cu(hd, waves);
+  const bool rot = waves >= 2 && per_cu >= 2 && (int64_t)grid.x * grid.y * grid.z <= 256LL * per_cu;
+#define SP_ATTN_CASE(HD_, W_)                                                                 \
+  if (hd == HD_ && waves == W_) {                                                             \
+    hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false>), grid, dim3(64 * W_), 0, s, p);       \
+    return hipGetLastError();                                                                 \
   }
-  SP_ATTN_CASE(128, 1) SP_ATTN_CASE(128, 2) SP_ATTN_CASE(128, 3) SP_ATTN_CASE(128, 4)
-  SP_ATTN_CASE(128, 5) SP_ATTN_CASE(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
+#define SP_ATTN_CASE_ROT(HD_, W_)                                                             \
+  if (hd == HD_ && waves == W_) {                                                             \
+    if (rot) hipLaunchKernelGGL((attn_split_bf16<HD_, W_, true>), grid, dim3(64 * W_), 0, s, p); \
+    else hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false>), grid, dim3(64 * W_), 0, s, p);    \
+    return hipGetLastError();                                                                 \
+  }
+  // rot can hold only where a compute unit takes two workgroups or more
+  SP_ATTN_CASE(128, 1) SP_ATTN_CASE_ROT(128, 2) SP_ATTN_CASE_ROT(128, 3) SP_ATTN_CASE_ROT(128, 4)
+  SP_ATTN_CASE_ROT(128, 5) SP_ATTN_CASE_ROT(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
   SP_ATTN_CASE(128, 12)
-  SP_ATTN_CASE(64, 1) SP_ATTN_CASE(64, 2) SP_ATTN_CASE(64, 3) SP_ATTN_CASE(64, 4)
-  SP_ATTN_CASE(64, 5) SP_ATTN_CASE(64, 6) SP_ATTN_CASE(64, 8) SP_ATTN_CASE(64, 10)
+  SP_ATTN_CASE(64, 1) SP_ATTN_CASE_ROT(64, 2) SP_ATTN_CASE_ROT(64, 3) SP_ATTN_CASE_ROT(64, 4)
+  SP_ATTN_CASE_ROT(64, 5) SP_ATTN_CASE_ROT(64, 6) SP_ATTN_CASE_ROT(64, 8) SP_ATTN_CASE_ROT(64, 10)
   SP_ATTN_CASE(64, 12) SP_ATTN_CASE(64, 16)
+#undef SP_ATTN_CASE_ROT
 #undef SP_ATTN_CASE
   return hipErrorInvalidValue;
 }

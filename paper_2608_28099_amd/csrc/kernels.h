@@ -65,6 +65,12 @@ struct AttnParams {
   int n_kv, rows, r_alloc, n_qgroups;
   int bs_log2, mbps, max_seq_len, split_len, max_splits;
 };
+// Workgroups of the bf16 attention kernel one compute unit holds: three by LDS,
+// and at most 12 waves (head_dim 128) or 20 (64) by VGPRs.
+inline int attn_wgs_per_cu(int hd, int waves) {
+  const int by_vgprs = (hd == 128 ? 12 : 20) / waves;
+  return by_vgprs < 3 ? by_vgprs : 3;
+}
 // Cache tokens only (the soft keys are folded in by the merge).
 // bf16-storage path (bf16 MFMA, split Q and P): head_dim 64/128, `waves` 16-row
 // query tiles per workgroup (1, 2, 3, 4, 5, 6, 8, 10 or 12; up to 16 for head_dim 64).

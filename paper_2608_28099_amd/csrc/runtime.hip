@@ -116,9 +116,7 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows) {
     // sequence: three splits for the longest sequences measured faster than
     // one, two or four on uniform and ragged batches alike, whether the grid
     // is one round or many.  At least 1024 tokens, a multiple of 256.
-    // Workgroups per compute unit: 3 by LDS, and at most 12 waves (head_dim
-    // 128) or 20 (64) by VGPRs.
-    const int64_t per_cu = std::min(3, (c.head_dim == 128 ? 12 : 20) / a.waves);
+    const int64_t per_cu = attn_wgs_per_cu(c.head_dim, a.waves);
     const int64_t slots = 256 * std::max<int64_t>(per_cu, 1);
     const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * a.n_qgroups;
     const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
