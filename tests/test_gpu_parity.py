@@ -7,6 +7,8 @@ bit: batch order, block placement, contiguous vs paged storage, repeated runs.
 """
 from __future__ import annotations
 
+import dataclasses
+
 import os
 
 import numpy as np
@@ -225,6 +227,30 @@ def test_invariances_are_bitwise(dev):
     kvp = inputs.permute_batch(kv_d, perm)
     out = probe.forward(kvp, p_d)
     assert torch.equal(out, base[perm]), "batch permutation changes the logits"
+    probe.close()
+
+
+def test_attention_is_independent_of_the_grid(dev):
+    """A sequence's attention output is the same bit for bit whether its launch
+    is one round of workgroups (the co-resident workgroups then rotate their wave
+    priorities) or several rounds (they do not): scheduling changes timing only."""
+    w = configs.Workload(name="grid_rounds", dtype="bf16", batch=48, k=16, hidden=256, n_q_heads=32,
+                         n_kv_heads=8, head_dim=128, intermediate=128, n_classes=2,
+                         seq_len=("uniform", 600, 1024), kv_std=1.0, weight_std=0.05, seed=71)
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w, split_len=256)
+    plan = probe.plan(w.batch)
+    assert plan["split_len"] == 256 and plan["max_splits"] == 4 and plan["query_groups"] == 1
+    n = 4 * w.k * w.n_q_heads * w.head_dim  # attention output of the first four sequences
+    # 8 KV heads x 4 splits x 48 sequences = 1536 four-wave workgroups: two rounds
+    probe.forward(kv_d, p_d)
+    many = probe.tap(binding.SP_TAP_ATTN, w.batch, dev).view(torch.float16)[:n].clone()
+    # the first four sequences alone: 128 workgroups, one round
+    bt = None if kv_d.block_table is None else kv_d.block_table[:4]
+    few_kv = dataclasses.replace(kv_d, block_table=bt, seq_lens=kv_d.seq_lens[:4])
+    probe.forward(few_kv, p_d)
+    few = probe.tap(binding.SP_TAP_ATTN, 4, dev).view(torch.float16)[:n].clone()
+    assert torch.equal(many, few), "the attention output depends on the grid"
     probe.close()
 
 
