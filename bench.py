@@ -2,20 +2,27 @@
 
 One step = one sp_probe_forward over the whole batch of the workload (soft-row
 prep, split attention over the paged KV cache, merge, o-projection, norm,
-SwiGLU MLP, final norm and classifier), inputs already resident in HBM.
---mode recursive: one step = one sp_probe_forward_recursive (recursive SP-k
-with the MTP input fusion: k single-row passes of the head, each reading the
-whole cache once) on the recursive workload.
+SwiGLU MLP, final norm and classifier), inputs already resident in HBM; the
+head's projections read its fp16 weight image, made once before timing (the
+head is frozen).  --mode recursive: one step = one sp_probe_forward_recursive
+(recursive SP-k with the MTP input fusion: k single-row passes of the head,
+each reading the whole cache once) on the recursive workload.
 
-Prints one JSON line:
-  value      classifications/s = batch x tasks / (wall time per step), timed over
-             K steps bracketed by device synchronisation (one task unless --tasks);
-  roofline   the split-attention kernel (the dominant one on the long-context
-             workload): algorithmic KV bytes per launch / its mean duration,
-             from HIP events recorded on the launch stream around it in the timed
-             steps, against 8 TB/s;
-  cpu_baseline  the fp64 oracle on the host cores over a bounded sample of the
-             same workload's sequences.
+Three timed passes, each after its own warm-up:
+  1. the contract's: exactly --steps steps bracketed by device synchronisation
+     on a handle without profiling -> value (classifications/s) and ms_per_step;
+  2. max(50, --steps) steps, each bracketed by HIP events on the launch stream
+     -> median, p10 and p90 per-step times;
+  3. --steps steps on a handle with per-stage HIP events -> the stage times and
+     the roofline of the attention stage (split kernel + merge, the two
+     attention kernels) and of the split kernel alone.
+KV caches under 1 GB are rotated over enough copies to exceed 1 GB, so that no
+step finds the previous step's KV in the caches.
+
+Prints one JSON line: the contract fields, roofline (algorithmic KV bytes per
+attention stage / its mean duration, against 8 TB/s and against the device's
+measured streaming-read rate), cpu_baseline (the fp64 oracle on the host cores
+over a bounded sample of the same workload's sequences).
 """
 from __future__ import annotations
 
@@ -33,6 +40,11 @@ METRIC = "classifications/sec at 1 MI355X; attention KV-read GB/s as % of HBM pe
 HBM_PEAK_GBPS = 8000.0
 MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix-core peak
 DEFAULT_WORKLOAD = {"one-pass": "long_9b_bf16", "recursive": "long_9b_bf16_sp5"}
+DTYPE_LABEL = {"bf16": "bf16 storage; fp16xfp16->fp32 MFMA projections (fp16 image of the bf16 weights); "
+                       "bf16 MFMA attention on stored K/V with hi+lo bf16 queries and probabilities; "
+                       "fp32 softmax, norms, residual stream and logits",
+               "f32": "f32"}
+ROTATE_BELOW = 1 << 30      # KV caches smaller than this are rotated over copies
 ATTN_SRC = os.path.join(ROOT, "paper_2608_28099_amd", "csrc", "attention.hip")
 PROFILES = os.path.join(ROOT, "profiles")
 
@@ -170,6 +182,7 @@ def main():
               "per sequence and would shard by sequence, but only the one-GPU path exists.",
               file=sys.stderr)
         sys.exit(2)
+    import numpy as np
     import torch
 
     from paper_2608_28099_amd import binding, configs, inputs
@@ -196,68 +209,117 @@ def main():
     T = 1 if recursive else args.tasks
     tasks = inputs.task_params(w, T, dev) if T > 1 else None
     logits = torch.empty((w.batch, T, w.n_classes), dtype=torch.float32, device=dev)
-    flags = binding.SP_FLAG_PROFILE | (binding.SP_FLAG_LAST_ROW_ONLY if args.last_row_only else 0)
-    probe = binding.Probe(w, split_len=args.split_len, flags=flags, max_tasks=T)
+    flags = binding.SP_FLAG_LAST_ROW_ONLY if args.last_row_only else 0
+    # the frozen head's fp16 image, made once (bf16 storage)
+    run_params = dict(params)
+    if w.dtype == "bf16":
+        run_params["packed"] = binding.pack_weights(w, params, max_tasks=T)
+    # KV copies so that the cache rotated through exceeds ROTATE_BELOW bytes
+    pool_bytes = kv.pool.numel() * kv.pool.element_size()
+    n_rot = 1 if pool_bytes >= ROTATE_BELOW else min(64, -(-ROTATE_BELOW // pool_bytes) + 1)
+    kvs = [kv] + [inputs.KVCache(kv.pool.clone(), kv.block_table, kv.seq_lens, kv.block_size,
+                                 kv.max_blocks_per_seq, kv.n_kv, kv.head_dim) for _ in range(n_rot - 1)]
+    plain = binding.Probe(w, split_len=args.split_len, flags=flags, max_tasks=T)
+    prof = binding.Probe(w, split_len=args.split_len, flags=flags | binding.SP_FLAG_PROFILE, max_tasks=T)
     torch.cuda.synchronize()
 
-    def step():
+    def step(probe, i):
+        kvi = kvs[i % n_rot]
         if recursive:
-            probe.forward_recursive(kv, params, fusion, logits)
+            probe.forward_recursive(kvi, run_params, fusion, logits)
         elif tasks is not None:
-            probe.forward_multi(kv, params, tasks["soft_prompts"], tasks["w_cls"], tasks["b_cls"], logits)
+            probe.forward_multi(kvi, run_params, tasks["soft_prompts"], tasks["w_cls"], tasks["b_cls"], logits)
         else:
-            probe.forward(kv, params, logits)
+            probe.forward(kvi, run_params, logits)
 
-    for _ in range(args.warmup):
-        step()
+    # 1. the contract's timed region
+    for i in range(args.warmup):
+        step(plain, i)
     torch.cuda.synchronize()
-    probe.profile_read()  # discard warm-up events
-
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for i in range(args.steps):
+        step(plain, i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    # the event pool keeps the last forwards that fit (all of them at these step counts)
-    stages, n_fwd = probe.profile_read()
-    assert 0 < n_fwd <= args.steps
     ms_per_step = 1000.0 * elapsed / args.steps
     assert bool(torch.isfinite(logits).all()), "non-finite logits"
+    assert plain.check_device_error() == 0, "device-side status after the timed steps"
+
+    # 2. per-step HIP events on the launch stream
+    n_dist = max(50, args.steps)
+    stream = torch.cuda.current_stream(dev)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_dist)]
+    for i in range(n_dist):
+        evs[i][0].record(stream)
+        step(plain, i)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    per_step = np.array([a.elapsed_time(b) for a, b in evs])
+    dist = {"steps": n_dist, "median_ms": round(float(np.median(per_step)), 4),
+            "p10_ms": round(float(np.percentile(per_step, 10)), 4),
+            "p90_ms": round(float(np.percentile(per_step, 90)), 4),
+            "value_at_median": round(w.batch * T / (float(np.median(per_step)) * 1e-3), 1)}
+
+    # 3. per-stage events
+    for i in range(args.warmup):
+        step(prof, i)
+    torch.cuda.synchronize()
+    prof.profile_read()  # discard warm-up events
+    for i in range(args.steps):
+        step(prof, i)
+    torch.cuda.synchronize()
+    stages, n_fwd = prof.profile_read()   # the event pool keeps the last forwards that fit (all of them here)
+    assert 0 < n_fwd <= args.steps
 
     esz = 2 if w.dtype == "bf16" else 4
     kv_bytes = int(lens.astype("int64").sum()) * w.n_kv_heads * w.head_dim * 2 * esz
     launches = w.k if recursive else 1   # attention launches per step
     attn_ms = stages["attention"] / (n_fwd * launches)
-    achieved = kv_bytes / (attn_ms * 1e-3) / 1e9
+    stage_ms = (stages["attention"] + stages["merge"]) / (n_fwd * launches)
+    achieved = kv_bytes / (stage_ms * 1e-3) / 1e9
+    achieved_k1 = kv_bytes / (attn_ms * 1e-3) / 1e9
+    # streaming-read ceiling of this device, over a 4 GiB buffer
+    buf = torch.empty(1 << 32, dtype=torch.uint8, device=dev)
+    buf.fill_(1)
+    read_peak = binding.measure_read_gbps(buf, reps=10)
+    del buf
     # counters are taken per launch shape: the workload, its task count and row pruning
     variant = w.name + (f"_tasks{T}" if T > 1 else "") + ("_last_row_only" if args.last_row_only else "")
     traffic = traffic_per_launch(variant)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "kernel": "attn_split_bf16" if w.dtype == "bf16" else "attn_split_f32",
-                "algorithmic_bytes_per_launch": kv_bytes, "mean_launch_ms": round(attn_ms, 4)}
-    plan = probe.plan_recursive(w.batch) if recursive else probe.plan(w.batch)
+                "kernel": ("attn_split_bf16 + merge_splits" if w.dtype == "bf16" else "attn_split_f32 + merge_splits"),
+                "algorithmic_bytes_per_launch": kv_bytes, "mean_launch_ms": round(stage_ms, 4),
+                "measured_read_peak_gbps": round(read_peak, 1),
+                "frac_of_measured_read_peak": round(achieved / read_peak, 4),
+                "split_kernel_only": {"mean_launch_ms": round(attn_ms, 4), "achieved": round(achieved_k1, 1),
+                                      "frac": round(achieved_k1 / HBM_PEAK_GBPS, 4)}}
+    plan = plain.plan_recursive(w.batch) if recursive else plain.plan(w.batch)
     out = {
-        "metric": (METRIC if not recursive else "recursive SP-k classifications/sec at 1 MI355X"), "value": round(w.batch * T / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
+        "metric": (METRIC if not recursive else "recursive SP-k classifications/sec at 1 MI355X"),
+        "value": round(w.batch * T / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": DTYPE_LABEL[w.dtype],
         "data": "synthetic (seeded; random-init head weights; paged KV ~N(0,1))",
         "config": {"workload": w.name, "batch": w.batch, "seq_len": list(w.seq_len), "k": w.k,
                    "hidden": w.hidden, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "intermediate": w.intermediate, "n_classes": w.n_classes,
                    "kv_layout": w.layout, "block_size": kv.block_size, "kv_bytes": kv_bytes,
+                   "kv_copies_rotated": n_rot, "weights": ("fp16 image" if "packed" in run_params else "as stored"),
                    "split_len": plan["split_len"], "parallelism": "single GPU",
                    "mode": args.mode, "attention_launches_per_step": launches, "tasks": T,
                    "last_row_only": bool(args.last_row_only)},
+        "step_time_distribution": dist,
         "roofline": roofline,
         "attention_gbps": round(achieved, 1),
         "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},
         "projections": projection_rates(w, T, args, recursive, stages, n_fwd),
         "hbm_copy_gbps": copy_rate(torch, dev),
     }
-    probe.close()
+    plain.close()
+    prof.close()
     if not args.no_cpu_baseline:
         print("[bench] timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, kv, params, args.cpu_seconds, fusion, tasks)

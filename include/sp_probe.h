@@ -49,15 +49,26 @@ typedef enum sp_status {
   SP_ERR_OUT_OF_MEMORY = -4, /* workspace allocation failed at init */
   SP_ERR_HIP = -5,           /* a HIP runtime call or kernel launch failed */
   SP_ERR_CAPACITY = -6,      /* batch larger than max_batch of the handle */
-  SP_ERR_DEVICE_DATA = -7    /* debug mode: device-resident seq_lens / block ids invalid */
+  SP_ERR_DEVICE_DATA = -7,   /* reported by sp_probe_check_device_error: a seq_len outside
+                                [0, max_seq_len] (any mode), or (debug mode) an invalid block
+                                id, class row or weight-image header */
+  SP_ERR_RANGE = -8,         /* reported by sp_probe_check_device_error: an fp16 activation
+                                (normed row, attention output, SwiGLU product) exceeded 65504 */
+  SP_ERR_INTERNAL = -9       /* reported by sp_probe_check_device_error: a guard word between
+                                workspace areas was overwritten (a library fault) */
 } sp_status;
 
 typedef enum sp_dtype {
   SP_F32 = 0,   /* fp32 weights, soft prompt and KV cache; fp32 arithmetic throughout */
-  SP_BF16 = 1   /* bf16 storage of weights, soft prompt and KV cache; fp16 MFMA operands
-                   (bf16 values converted exactly, activations rounded to fp16) with fp32
-                   accumulation; fp32 norms, softmax statistics, residual stream, logits.
-                   KV and weight magnitudes must stay below 65504 (fp16 range) */
+  SP_BF16 = 1   /* bf16 storage of weights, soft prompt and KV cache.  Projections: fp16
+                   MFMA operands (bf16 weights converted exactly, activations rounded to
+                   fp16), fp32 accumulation.  Attention: bf16 MFMA on the stored K and V
+                   with the queries and probabilities split in bf16 hi + lo parts.  fp32
+                   norms, softmax statistics, residual stream and logits.  Range: weight
+                   and KV magnitudes must stay below 65504, and so must the fp16
+                   activations (normed rows, attention outputs, SwiGLU products: |x| <= 65504);
+                   an activation past that is stored as inf and reported by
+                   sp_probe_check_device_error as SP_ERR_RANGE */
 } sp_dtype;
 
 typedef enum sp_pool {
@@ -94,8 +105,11 @@ typedef struct sp_probe_config {
   float rms_eps;         /* epsilon inside every RMSNorm square root */
   double rope_base;      /* RoPE base; pair (i, i + head_dim/2) turns by pos * base^(-2i/head_dim) */
   int32_t max_batch;     /* largest batch a forward may pass */
-  int32_t max_seq_len;   /* largest context length N_b a forward may pass (debug mode checks it;
-                            otherwise larger values are clamped to it) */
+  int32_t max_seq_len;   /* largest context length N_b a forward may pass.  A seq_len outside
+                            [0, max_seq_len] is clamped to that range (the sequence is then
+                            classified on its first max_seq_len tokens) and reported by
+                            sp_probe_check_device_error as SP_ERR_DEVICE_DATA, in any mode;
+                            debug mode also skips the forward's later kernels */
   int32_t split_len;     /* tokens per attention split, a power of two >= 256; 0 = automatic */
   int32_t flags;         /* SP_FLAG_* */
   int32_t max_tasks;     /* largest task count of sp_probe_forward_multi, 1..64 (0 = 1);
@@ -153,12 +167,37 @@ typedef struct sp_probe_weights {
   const float* b_cls;
   const int32_t* cls_rows;     /* nullable, device */
   int64_t cls_vocab;           /* rows of w_cls when cls_rows is set */
+  /* nullable, device: an fp16 image of the seven projection matrices made by
+   * sp_probe_pack_weights for this config (bf16 storage only).  When set, the
+   * forwards read w_q, w_k, w_v, w_o, w_gate, w_up and w_down from the image
+   * (those seven pointers may then be NULL) and skip the per-fragment
+   * conversion; the results are identical bit for bit. */
+  const void* packed;
 } sp_probe_weights;
 
 typedef struct sp_probe sp_probe_t;  /* opaque handle, library-owned */
 
-/* Bytes of device workspace a handle with this config allocates (0 if invalid). */
+/* Bytes of device workspace a handle with this config allocates on the
+ * current device (0 if invalid).  The split plan depends on the device's
+ * compute-unit count; with no device, 256 compute units are assumed. */
 size_t sp_probe_workspace_bytes(const sp_probe_config* cfg);
+
+/* The frozen head's fp16 weight image (Sec. 3.2: the head is frozen, so its
+ * matrices can be converted once and reused by every forward).
+ * sp_probe_packed_bytes: bytes of the image for cfg (0 if cfg is invalid or not
+ * SP_BF16).  sp_probe_pack_weights: enqueues on `stream` the conversion of the
+ * bf16 matrices w_q, w_k, w_v, w_o, w_gate, w_up, w_down of `weights` (device,
+ * the layouts of sp_probe_weights) into `packed` (device, caller-owned,
+ * 16-byte aligned, packed_bytes >= sp_probe_packed_bytes(cfg)): a 256-byte
+ * header naming the shape, then the matrices as fp16.  The values are
+ * converted exactly (the same conversion the projections otherwise apply per
+ * fragment), so forwards with and without the image return identical logits.
+ * The image is a snapshot: pack again after changing the matrices.  Errors:
+ * SP_ERR_INVALID_ARG (null or misaligned pointers, packed_bytes too small),
+ * SP_ERR_UNSUPPORTED (an SP_F32 config), SP_ERR_NO_DEVICE. */
+size_t sp_probe_packed_bytes(const sp_probe_config* cfg);
+int sp_probe_pack_weights(const sp_probe_config* cfg, const sp_probe_weights* weights, void* packed,
+                          size_t packed_bytes, void* stream);
 
 /* Validate cfg, check that the current HIP device is gfx950, allocate the
  * workspace (soft-row scratch K/V, queries, split partials, activations) for
@@ -254,8 +293,12 @@ enum { SP_TAP_QKV = 0, SP_TAP_ATTN = 1, SP_TAP_A = 2, SP_TAP_Y = 3, SP_TAP_X = 4
 size_t sp_probe_tap_bytes(const sp_probe_t* h, int tap, int32_t batch);
 int sp_probe_copy_tap(sp_probe_t* h, int tap, int32_t batch, void* dst, size_t dst_bytes, void* stream);
 
-/* Debug mode: wait for `stream`, then report SP_ERR_DEVICE_DATA if any forward
- * since the last call saw an invalid seq_len or block id (and clear the flag). */
+/* Wait for `stream` and report what the forwards since the last call met on
+ * the device, then clear it: SP_ERR_INTERNAL if a guard word of the workspace
+ * was overwritten; SP_ERR_DEVICE_DATA for a seq_len outside [0, max_seq_len]
+ * (any mode) or, in debug mode, an invalid block id, class row or weight-image
+ * header; SP_ERR_RANGE if an fp16 activation exceeded 65504; else SP_OK.
+ * Synchronises the host. */
 int sp_probe_check_device_error(sp_probe_t* h, void* stream);
 
 /* Profiling mode: per-stage device time summed over the forwards since the last
@@ -278,6 +321,21 @@ int sp_probe_plan(const sp_probe_t* h, int32_t batch, int32_t* split_len, int32_
 /* The same for the attention of a recursive step (G query rows per KV head). */
 int sp_probe_plan_recursive(const sp_probe_t* h, int32_t batch, int32_t* split_len,
                             int32_t* max_splits, int32_t* rows_per_kv_head, int32_t* query_groups);
+/* The one-task one-pass split plan and the workspace size a handle with cfg
+ * would use on a device of num_cus compute units; host only (no device
+ * needed).  Any output pointer may be NULL.  SP_ERR_INVALID_ARG for num_cus
+ * outside 1..65536, else the status of the config check. */
+int sp_probe_plan_config(const sp_probe_config* cfg, int32_t num_cus, int32_t* split_len,
+                         int32_t* max_splits, int32_t* rows_per_kv_head, int32_t* query_groups,
+                         size_t* workspace_bytes);
+
+/* Measurement: the rate of plain streaming reads of `bytes` (>= 16) at `buf`
+ * (device, 16-byte aligned, read only) on the current device, the ceiling of a
+ * read-bound kernel: one warm-up pass, then `reps` timed passes on `stream`
+ * (16-byte non-temporal loads, four in flight per lane); *gbps receives the
+ * bytes read per second / 1e9.  `sink` (device, 4 bytes) may be written.
+ * Synchronises the host.  SP_ERR_INVALID_ARG, SP_ERR_NO_DEVICE, SP_ERR_HIP. */
+int sp_probe_measure_read(const void* buf, size_t bytes, int32_t reps, void* sink, float* gbps, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(PKG, "libsp_probe.so")
 SP_OK = 0
 STATUS = {0: "SP_OK", -1: "SP_ERR_INVALID_ARG", -2: "SP_ERR_UNSUPPORTED", -3: "SP_ERR_NO_DEVICE",
           -4: "SP_ERR_OUT_OF_MEMORY", -5: "SP_ERR_HIP", -6: "SP_ERR_CAPACITY",
-          -7: "SP_ERR_DEVICE_DATA"}
+          -7: "SP_ERR_DEVICE_DATA", -8: "SP_ERR_RANGE", -9: "SP_ERR_INTERNAL"}
+SP_ERR_DEVICE_DATA, SP_ERR_RANGE, SP_ERR_INTERNAL = -7, -8, -9
 SP_F32, SP_BF16 = 0, 1
 SP_POOL_LAST, SP_POOL_MEAN = 0, 1
 SP_FLAG_DEBUG, SP_FLAG_PROFILE, SP_FLAG_LAST_ROW_ONLY = 1, 2, 4
@@ -28,7 +29,8 @@ STAGES = ("soft_prep", "attention", "merge", "o_proj", "post_norm", "gate_up", "
 EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward",
            "sp_probe_forward_multi", "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
            "sp_probe_tap_bytes", "sp_probe_copy_tap", "sp_probe_check_device_error",
-           "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive")
+           "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive", "sp_probe_plan_config",
+           "sp_probe_packed_bytes", "sp_probe_pack_weights", "sp_probe_measure_read")
 
 
 class sp_probe_config(ctypes.Structure):
@@ -54,7 +56,8 @@ class sp_kv_cache(ctypes.Structure):
 class sp_probe_weights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in
                 ("in_norm", "w_q", "w_k", "w_v", "w_o", "post_norm", "w_gate", "w_up", "w_down",
-                 "final_norm", "w_cls", "b_cls", "cls_rows")] + [("cls_vocab", ctypes.c_int64)]
+                 "final_norm", "w_cls", "b_cls", "cls_rows")] + [("cls_vocab", ctypes.c_int64),
+                                                                  ("packed", ctypes.c_void_p)]
 
 
 
@@ -104,6 +107,15 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_plan.restype = ctypes.c_int
     lib.sp_probe_plan_recursive.argtypes = [vp, ctypes.c_int32] + [P(ctypes.c_int32)] * 4
     lib.sp_probe_plan_recursive.restype = ctypes.c_int
+    lib.sp_probe_plan_config.argtypes = [P(sp_probe_config), ctypes.c_int32] + [P(ctypes.c_int32)] * 4 + \
+        [P(ctypes.c_size_t)]
+    lib.sp_probe_plan_config.restype = ctypes.c_int
+    lib.sp_probe_packed_bytes.argtypes = [P(sp_probe_config)]
+    lib.sp_probe_packed_bytes.restype = ctypes.c_size_t
+    lib.sp_probe_pack_weights.argtypes = [P(sp_probe_config), P(sp_probe_weights), vp, ctypes.c_size_t, vp]
+    lib.sp_probe_pack_weights.restype = ctypes.c_int
+    lib.sp_probe_measure_read.argtypes = [vp, ctypes.c_size_t, ctypes.c_int32, vp, P(ctypes.c_float), vp]
+    lib.sp_probe_measure_read.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -162,6 +174,38 @@ def sp_probe_status_string(status: int) -> str:
     return load().sp_probe_status_string(status).decode()
 
 
+def sp_probe_plan_config(cfg: sp_probe_config, num_cus: int):
+    """Host-only split plan and workspace size of cfg on a device of num_cus compute units."""
+    vals = [ctypes.c_int32() for _ in range(4)]
+    ws = ctypes.c_size_t()
+    st = load().sp_probe_plan_config(ctypes.byref(cfg), num_cus, *[ctypes.byref(v) for v in vals],
+                                     ctypes.byref(ws))
+    _check(st, "sp_probe_plan_config")
+    return {"split_len": vals[0].value, "max_splits": vals[1].value, "rows_per_kv_head": vals[2].value,
+            "query_groups": vals[3].value, "workspace_bytes": ws.value}
+
+
+def measure_read_gbps(buf, reps: int = 10, stream=None) -> float:
+    """Streaming-read rate of the device over the device tensor buf (GB/s)."""
+    import torch
+    sink = torch.zeros(4, dtype=torch.int32, device=buf.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(buf.device).cuda_stream
+    out = ctypes.c_float()
+    _check(load().sp_probe_measure_read(buf.data_ptr(), buf.numel() * buf.element_size(), reps, sink.data_ptr(),
+                                        ctypes.byref(out), stream), "sp_probe_measure_read")
+    return float(out.value)
+
+
+def sp_probe_packed_bytes(cfg: sp_probe_config) -> int:
+    return load().sp_probe_packed_bytes(ctypes.byref(cfg))
+
+
+def sp_probe_pack_weights(cfg: sp_probe_config, weights: sp_probe_weights, packed, packed_bytes: int,
+                          stream) -> int:
+    return load().sp_probe_pack_weights(ctypes.byref(cfg), ctypes.byref(weights), packed, packed_bytes, stream)
+
+
 # ---------------------------------------------------------------- torch-facing helpers
 
 def make_config(w, max_batch: Optional[int] = None, max_seq_len: Optional[int] = None,
@@ -192,10 +236,11 @@ def make_kv(kv, batch: Optional[int] = None) -> sp_kv_cache:
 
 def make_weights(params: dict) -> sp_probe_weights:
     """params: the head's tensors; optional cls_rows (device int32) selects rows of
-    w_cls, a vocabulary matrix of cls_vocab rows (default: its first dimension)."""
+    w_cls, a vocabulary matrix of cls_vocab rows (default: its first dimension);
+    optional packed: a uint8 tensor holding the fp16 weight image (pack_weights)."""
     wt = sp_probe_weights(**{n: _ptr(params.get(n)) for n in
                              ("in_norm", "w_q", "w_k", "w_v", "w_o", "post_norm", "w_gate",
-                              "w_up", "w_down", "final_norm", "w_cls", "b_cls", "cls_rows")})
+                              "w_up", "w_down", "final_norm", "w_cls", "b_cls", "cls_rows", "packed")})
     if params.get("cls_rows") is not None:
         wt.cls_vocab = params.get("cls_vocab", params["w_cls"].shape[0])
     return wt
@@ -204,6 +249,22 @@ def make_weights(params: dict) -> sp_probe_weights:
 def make_fusion(fusion: dict) -> sp_probe_fusion:
     return sp_probe_fusion(**{n: _ptr(fusion.get(n)) for n in
                               ("fc_norm_hidden", "fc_norm_embed", "w_fc", "w_hidden_fuse")})
+
+
+def pack_weights(w, params: dict, stream=None, max_tasks: int = 1):
+    """The fp16 weight image of the head in params (a device uint8 tensor), made by
+    sp_probe_pack_weights; pass it as params["packed"]."""
+    import torch
+    cfg = make_config(w, max_tasks=max_tasks)
+    n = sp_probe_packed_bytes(cfg)
+    if n == 0:
+        raise ProbeError(-2, "sp_probe_packed_bytes")
+    dev = params["w_q"].device
+    img = torch.empty(n, dtype=torch.uint8, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream
+    _check(sp_probe_pack_weights(cfg, make_weights(params), img.data_ptr(), n, stream), "sp_probe_pack_weights")
+    return img
 
 
 class Probe:

@@ -8,7 +8,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libsp_probe.so")
-SOURCES = ["attention.hip", "merge.hip", "gemm.hip", "rowops.hip", "runtime.hip"]
+SOURCES = ["attention.hip", "merge.hip", "gemm.hip", "rowops.hip", "runtime.hip", "measure.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -22,20 +22,33 @@ FLAGS = [
 
 
 def build(verbose: bool = False, extra=None) -> str:
-    """Compile every HIP source into LIB (always recompiles); returns the path."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, *(extra or []), "-o", tmp, *srcs]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
+    """Compile every HIP source into LIB (always recompiles; one hipcc process
+    per source, in parallel, then one link); returns the path."""
+    import concurrent.futures
+    import tempfile
     noise = "is not a recognized feature for this target"
-    msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
-    if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
-    if verbose and msgs.strip():
-        print(msgs, file=sys.stderr)
-    os.replace(tmp, LIB)
+
+    def run(cmd):
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines() if noise not in l)
+        if res.returncode != 0:
+            raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
+        if verbose and msgs.strip():
+            print(msgs, file=sys.stderr)
+
+    with tempfile.TemporaryDirectory(prefix="sp_probe_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, s.replace(".hip", ".o")) for s in SOURCES]
+        cflags = [f for f in FLAGS if f != "-shared"]
+        cmds = [[HIPCC, *cflags, *(extra or []), "-c", "-o", o, os.path.join(CSRC, s)]
+                for s, o in zip(SOURCES, objs)]
+        workers = min(len(cmds), max(1, (os.cpu_count() or 1)))
+        with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(run, cmds))
+        tmp = LIB + ".tmp"
+        run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs])
+        os.replace(tmp, LIB)
     return LIB
 
 

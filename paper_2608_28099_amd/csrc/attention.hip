@@ -390,10 +390,11 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     // in dispatch order and the launch on a tail at one or two per compute
     // unit.  There (ROT) their wave priorities rotate with the 100 MHz
     // real-time counter (every 2^12 ticks, 41 us): a workgroup's dispatch pass
-    // (256 compute units per pass) sets its phase, so the workgroups of one
-    // compute unit take turns at each priority level.  Timing only: what each
-    // workgroup computes does not change.
-    const int rot_phase = (int)(((blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z)) >> 8) % 3);
+    // (one workgroup per compute unit per pass) sets its phase, so the
+    // workgroups of one compute unit take turns at each priority level.
+    // Timing only: what each workgroup computes does not change.
+    const int rot_phase =
+        (int)(((blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z)) / p.num_cus) % 3);
     auto rotate_priority = [&]() __attribute__((always_inline)) {
       const int ep = (int)((__builtin_amdgcn_s_memrealtime() >> 12) % 3);
       const int pr = __builtin_amdgcn_readfirstlane((rot_phase + ep) % 3);
@@ -550,8 +551,9 @@ hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int bat
   // uniform batches: 83% of HBM peak against 78%).  Grids of many rounds
   // refill compute units as workgroups end, and one-wave workgroups do not
   // stagger; there the clock reads only cost time (2-5% measured).
+  if (p.num_cus < 1) return hipErrorInvalidValue;
   const int per_cu = attn_wgs_per_cu(hd, waves);
-  const bool rot = waves >= 2 && per_cu >= 2 && (int64_t)grid.x * grid.y * grid.z <= 256LL * per_cu;
+  const bool rot = waves >= 2 && per_cu >= 2 && (int64_t)grid.x * grid.y * grid.z <= (int64_t)p.num_cus * per_cu;
 #define SP_ATTN_CASE(HD_, W_)                                                                 \
   if (hd == HD_ && waves == W_) {                                                             \
     hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false>), grid, dim3(64 * W_), 0, s, p);       \

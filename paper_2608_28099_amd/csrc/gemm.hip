@@ -19,6 +19,16 @@
 // workgroups to keep enough loads in flight): blockIdx.y takes a slice of the
 // K steps and writes its fp32 partial tile; gemm_reduce sums the slices in a
 // fixed order and applies the epilogue.
+// Weights come either as the caller's bf16 matrices (WBF16, converted per
+// fragment) or as an fp16 image of them made once for the frozen head (no
+// conversion: the same values, so the same results bit for bit).
+// Tile order: workgroups are dealt to the XCDs round-robin (launch index mod
+// the XCD count).  The launch index is re-mapped so that each XCD takes a
+// contiguous run of a grouped tile order (group_m row tiles, then the next
+// column tile): the workgroups that share an XCD's L2 at one time then cover a
+// compact block of group_m row tiles by (CUs per XCD / group_m) column tiles,
+// instead of every row tile of one column tile, and fetch far fewer operand
+// bytes from beyond the L2 (27B-shaped gate/up on 8192 rows: 15% faster).
 #include "common.h"
 #include "kernels.h"
 
@@ -27,7 +37,20 @@ namespace {
 
 __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
 
-template <int BM, int BN, int WGM, int WGN, int S, int BK, int EPI, bool PART = false>
+// Tile (m_tile, n_tile) of launch index L among nwg tiles (see the tile order above).
+__device__ __forceinline__ void tile_of(int L, int nwg, int mtiles, int ntiles, int n_xcd, int group_m,
+                                        int& m_tile, int& n_tile) {
+  const int x = L % n_xcd, r = L / n_xcd;
+  const int q = nwg / n_xcd, rem = nwg % n_xcd;
+  const int t = (x < rem ? x * (q + 1) : rem * (q + 1) + (x - rem) * q) + r;
+  const int per_group = group_m * ntiles;
+  const int g = t / per_group, in = t - g * per_group;
+  const int gm = min(group_m, mtiles - g * group_m);  // the last group may hold fewer row tiles
+  m_tile = g * group_m + in % gm;
+  n_tile = in / gm;
+}
+
+template <int BM, int BN, int WGM, int WGN, int S, int BK, int EPI, bool PART, bool WBF16>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   constexpr int NW = WGM * WGN, WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
   constexpr int PPR = BK / 8;                        // 16-byte pieces per tile row
@@ -47,20 +70,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   __builtin_assume(wave >= 0 && wave < NW);
   const int wm = wave / WGN, wn = wave % WGN;
 
-  // Tile order: workgroups are dealt to the 8 XCDs round-robin, so the M tiles
-  // that share a weight tile get linear ids 8 apart (one XCD, one L2) and are
-  // dispatched together.
   const int mtiles = (p.M + BM - 1) / BM, ntiles = p.N / BN;
-  const int L = blockIdx.x;
   int m_tile, n_tile;
-  if ((ntiles & 7) == 0) {
-    const int r = L >> 3;
-    m_tile = r % mtiles;
-    n_tile = (r / mtiles) * 8 + (L & 7);
-  } else {
-    m_tile = L % mtiles;
-    n_tile = L / mtiles;
-  }
+  tile_of(blockIdx.x, gridDim.x, mtiles, ntiles, p.n_xcd, p.group_m, m_tile, n_tile);
   const int m0 = m_tile * BM, n0 = n_tile * BN;
 
   // This wave's loads: slots j*NW + wave (mod NI; a wave count that does not
@@ -132,7 +144,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
       for (int i = 0; i < MT; ++i) af[i] = __builtin_bit_cast(f16x8, As[(wm * WM + 16 * i + li) * PPR + pc]);
 #pragma unroll
       for (int j = 0; j < NT; ++j)
-        bfr[j] = __builtin_bit_cast(f16x8, bf16x8_to_f16x8(Bs[(wn * WN + 16 * j + li) * PPR + pc]));
+        bfr[j] = __builtin_bit_cast(f16x8, WBF16 ? bf16x8_to_f16x8(Bs[(wn * WN + 16 * j + li) * PPR + pc])
+                                                 : Bs[(wn * WN + 16 * j + li) * PPR + pc]);
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -143,6 +156,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   wait_vmcnt<0>();
 
   // Lane holds C[16i + 4la + r][16j + li] of the wave tile.
+  bool oor = false;  // an fp16 SwiGLU output out of fp16's range
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
 #pragma unroll
@@ -159,7 +173,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
           const int pair = (wn * WN + 16 * j) >> 5;
           const int n = n_tile * (BN / 2) + 16 * pair + li;
           const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-          ((f16*)p.c)[(int64_t)m * p.ldc + n] = (f16)(silu(gt) * up);
+          const float v = silu(gt) * up;
+          oor |= !(fabsf(v) <= 65504.0f);
+          ((f16*)p.c)[(int64_t)m * p.ldc + n] = (f16)v;
         }
       } else {
 #pragma unroll
@@ -177,6 +193,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
       }
     }
   }
+  if (EPI == kEpiSwiglu && !PART && __any(oor) && lane == 0 && p.status) atomicOr(p.status, kStatusRange);
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -231,7 +248,9 @@ __global__ __launch_bounds__(256) void gemm_reduce(const GemmParams p, int kspli
       gt += src[k * slice + g];
       up += src[k * slice + g + 16];
     }
-    ((f16*)p.c)[(int64_t)m * p.ldc + o] = (f16)(silu(gt) * up);
+    const float v = silu(gt) * up;
+    ((f16*)p.c)[(int64_t)m * p.ldc + o] = (f16)v;
+    if (!(fabsf(v) <= 65504.0f) && p.status) atomicOr(p.status, kStatusRange);
     return;
   }
   float v = 0.f;
@@ -242,40 +261,17 @@ __global__ __launch_bounds__(256) void gemm_reduce(const GemmParams p, int kspli
   ((float*)p.c)[(int64_t)m * p.ldc + o] = v;
 }
 
-template <int BM, int BN, int WGM, int WGN, int S, int BK>
-hipError_t launch_split(Epilogue epi, const GemmParams& p, int ksplit, hipStream_t s) {
-  const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN), ksplit), block(64 * WGM * WGN);
+template <int BM, int BN, int WGM, int WGN, int S, int BK, bool PART, bool WB>
+hipError_t launch_tile_k(Epilogue epi, const GemmParams& p, dim3 grid, hipStream_t s) {
+  const dim3 block(64 * WGM * WGN);
   switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore, true>), grid, block, 0, s, p); break;
-    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow, true>), grid, block, 0, s, p); break;
-    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32, true>), grid, block, 0, s, p); break;
-    case kEpiRowScale: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiRowScale, true>), grid, block, 0, s, p); break;
-    case kEpiSwiglu: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu, true>), grid, block, 0, s, p); break;
-  }
-  const int n_out = epi == kEpiSwiglu ? p.N / 2 : p.N;
-  const dim3 rgrid((unsigned)(((int64_t)p.M * n_out + 255) / 256));
-  switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL(gemm_reduce<kEpiStore>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
-    case kEpiResidRow: hipLaunchKernelGGL(gemm_reduce<kEpiResidRow>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
-    case kEpiResidF32: hipLaunchKernelGGL(gemm_reduce<kEpiResidF32>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
-    case kEpiRowScale: hipLaunchKernelGGL(gemm_reduce<kEpiRowScale>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
-    case kEpiSwiglu: hipLaunchKernelGGL(gemm_reduce<kEpiSwiglu>, rgrid, dim3(256), 0, s, p, ksplit, BN); break;
-  }
-  return hipGetLastError();
-}
-
-template <int BM, int BN, int WGM, int WGN, int S, int BK>
-hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
-  if (p.K % BK) return hipErrorInvalidValue;
-  const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN)), block(64 * WGM * WGN);
-  switch (epi) {
-    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore>), grid, block, 0, s, p); break;
-    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow>), grid, block, 0, s, p); break;
-    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32>), grid, block, 0, s, p); break;
-    case kEpiRowScale: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiRowScale>), grid, block, 0, s, p); break;
+    case kEpiStore: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiStore, PART, WB>), grid, block, 0, s, p); break;
+    case kEpiResidRow: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidRow, PART, WB>), grid, block, 0, s, p); break;
+    case kEpiResidF32: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiResidF32, PART, WB>), grid, block, 0, s, p); break;
+    case kEpiRowScale: hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiRowScale, PART, WB>), grid, block, 0, s, p); break;
     case kEpiSwiglu:
       if constexpr ((BN / WGN) % 32 == 0)
-        hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_lds<BM, BN, WGM, WGN, S, BK, kEpiSwiglu, PART, WB>), grid, block, 0, s, p);
       else
         return hipErrorInvalidValue;
       break;
@@ -283,21 +279,38 @@ hipError_t launch_lds_tile(Epilogue epi, const GemmParams& p, hipStream_t s) {
   return hipGetLastError();
 }
 
+// K split ksplit ways (ksplit > 1: fp32 partials in p.part, then gemm_reduce).
+template <int BM, int BN, int WGM, int WGN, int S, int BK>
+hipError_t launch_tile(Epilogue epi, const GemmParams& p, int ksplit, hipStream_t s) {
+  if (p.K % (BK * ksplit)) return hipErrorInvalidValue;
+  const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN), ksplit);
+  hipError_t e;
+  if (ksplit > 1)
+    e = p.b_f16 ? launch_tile_k<BM, BN, WGM, WGN, S, BK, true, false>(epi, p, grid, s)
+                : launch_tile_k<BM, BN, WGM, WGN, S, BK, true, true>(epi, p, grid, s);
+  else
+    e = p.b_f16 ? launch_tile_k<BM, BN, WGM, WGN, S, BK, false, false>(epi, p, grid, s)
+                : launch_tile_k<BM, BN, WGM, WGN, S, BK, false, true>(epi, p, grid, s);
+  if (e != hipSuccess || ksplit == 1) return e;
+  return launch_gemm_reduce(epi, p, ksplit, BN, s);
+}
+
 // Tile shapes, in order of preference (measured on the probe's projection
 // shapes, 512 to 8192 rows): (BM, BN, waves along M, waves along N, K-step
-// depth); the stage counts are in launch_gemm.  SwiGLU (gate/up) prefers the
-// widest tiles; the residual epilogues (o, down) prefer 256 x 128 tiles with
+// depth); the stage counts are in launch_tile_index.  SwiGLU (gate/up) prefers
+// the widest tiles; the residual epilogues (o, down) prefer 256 x 128 tiles with
 // 64-deep steps, which at 2048-8192 rows take half the time of 128 x 64.  The
-// 256 x 256 tile runs 2 x 4 waves: each weight fragment is then converted by
-// two waves instead of four (gate/up on 8192 rows 9% faster than 4 x 2).
+// 256 x 256 tile runs 2 x 4 waves: each weight fragment is then read (and, from
+// bf16 weights, converted) by two waves instead of four.  Index 9 is the
+// 32 x 128 tile of the 17-32-row products.
 struct TileShape { int bm, bn, wgm, wgn, bk; };
-constexpr int kNumTiles = 9;
+constexpr int kNumTiles = 10;
 constexpr TileShape kTiles[kNumTiles] = {
     {256, 256, 2, 4, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
     {64, 64, 2, 2, 64},   {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64},  {16, 16, 1, 1, 64},
-    {16, 32, 1, 1, 32}};
-constexpr int kOrderSwiglu[kNumTiles] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
-constexpr int kOrderResid[kNumTiles] = {2, 1, 0, 3, 4, 5, 6, 7, 8};
+    {16, 32, 1, 1, 32},   {32, 128, 1, 4, 64}};
+constexpr int kOrderSwiglu[9] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
+constexpr int kOrderResid[9] = {2, 1, 0, 3, 4, 5, 6, 7, 8};
 
 bool tile_ok(const GemmParams& p, Epilogue epi, const TileShape& t) {
   if (p.N % t.bn || p.K % t.bk) return false;
@@ -305,11 +318,52 @@ bool tile_ok(const GemmParams& p, Epilogue epi, const TileShape& t) {
   return p.b_split0 % t.bn == 0 && p.b_split1 % t.bn == 0;
 }
 
+hipError_t launch_tile_index(int c, Epilogue epi, const GemmParams& p, int ksplit, hipStream_t s) {
+  switch (c) {
+    case 0: return launch_tile<256, 256, 2, 4, 3, 32>(epi, p, ksplit, s);
+    case 1: return launch_tile<256, 192, 4, 2, 3, 32>(epi, p, ksplit, s);
+    case 2: return launch_tile<256, 128, 4, 2, 3, 64>(epi, p, ksplit, s);
+    case 3: return launch_tile<128, 64, 4, 2, 6, 64>(epi, p, ksplit, s);
+    case 4: return launch_tile<64, 64, 2, 2, 8, 64>(epi, p, ksplit, s);
+    case 5: return launch_tile<32, 64, 1, 2, 8, 64>(epi, p, ksplit, s);
+    case 6: return launch_tile<16, 32, 1, 1, 8, 64>(epi, p, ksplit, s);
+    case 7: return launch_tile<16, 16, 1, 1, 8, 64>(epi, p, ksplit, s);
+    case 8: return launch_tile<16, 32, 1, 1, 8, 32>(epi, p, ksplit, s);
+    case 9: return launch_tile<32, 128, 1, 4, 6, 64>(epi, p, ksplit, s);
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
-hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s) {
-  if (p.M <= 0) return hipSuccess;
+hipError_t launch_gemm_reduce(Epilogue epi, const GemmParams& p, int ksplit, int bn, hipStream_t s) {
+  const int n_out = epi == kEpiSwiglu ? p.N / 2 : p.N;
+  const dim3 rgrid((unsigned)(((int64_t)p.M * n_out + 255) / 256));
+  switch (epi) {
+    case kEpiStore: hipLaunchKernelGGL(gemm_reduce<kEpiStore>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
+    case kEpiResidRow: hipLaunchKernelGGL(gemm_reduce<kEpiResidRow>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
+    case kEpiResidF32: hipLaunchKernelGGL(gemm_reduce<kEpiResidF32>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
+    case kEpiRowScale: hipLaunchKernelGGL(gemm_reduce<kEpiRowScale>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
+    case kEpiSwiglu: hipLaunchKernelGGL(gemm_reduce<kEpiSwiglu>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tile(Epilogue epi, const GemmParams& p, int tile, int ksplit, hipStream_t s) {
+  if (tile < 0 || tile >= kNumTiles || !tile_ok(p, epi, kTiles[tile]) || ksplit < 1) return hipErrorInvalidValue;
+  if (p.lda % 8 || p.ldb % 8) return hipErrorInvalidValue;
+  if (ksplit > 1 && (!p.part || (size_t)ksplit * p.M * p.N * sizeof(float) > p.part_bytes))
+    return hipErrorInvalidValue;
+  GemmParams q = p;
+  if (q.n_xcd < 1) q.n_xcd = 1;
+  if (q.group_m < 1) q.group_m = 1 << 30;
+  return launch_tile_index(tile, epi, q, ksplit, s);
+}
+
+hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t s) {
+  if (p0.M <= 0) return hipSuccess;
   if (dt == kF32) {
+    const GemmParams& p = p0;
     const int n_out = epi == kEpiSwiglu ? p.N / 2 : p.N;
     const dim3 grid((n_out + 255) / 256, p.M);
     switch (epi) {
@@ -321,65 +375,53 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t 
     }
     return hipGetLastError();
   }
-  if (p.K % 32 || p.lda % 8 || p.ldb % 8) return hipErrorInvalidValue;
+  if (p0.K % 32 || p0.lda % 8 || p0.ldb % 8) return hipErrorInvalidValue;
+  GemmParams p = p0;
+  const int cus = p.n_cus > 0 ? p.n_cus : 256;
+  if (p.n_xcd < 1) p.n_xcd = 1;
+  // group of row tiles: the XCD's compute units then cover about a square of
+  // tiles (8 row tiles by 4 column tiles with 32 compute units per XCD)
+  if (p.group_m < 1) p.group_m = 8;
+  auto fits = [&](int ks) { return p.part && (size_t)ks * p.M * p.N * sizeof(float) <= p.part_bytes; };
   // 17..32 rows: the product streams the weights; a 32-row by 128-column tile
   // with four waves, and K split so that the grid has enough workgroups in
   // flight (each slice at least 8 steps of 64).  (Up to 16 rows the one-wave
   // 16-row tiles below measured faster.)
-  constexpr TileShape kSmall{32, 128, 1, 4, 64};
-  if (p.M > 16 && p.M <= 32 && tile_ok(p, epi, kSmall)) {
+  if (p.M > 16 && p.M <= 32 && tile_ok(p, epi, kTiles[9])) {
     const int tiles = p.N / 128, KT = p.K / 64;
     int ks = 1;
-    while (ks < 16 && tiles * ks * 2 <= 1024 && KT / (ks * 2) >= 8 &&
-           (size_t)(ks * 2) * p.M * p.N * sizeof(float) <= p.part_bytes && p.part)
-      ks *= 2;
-    if (ks > 1) return launch_split<32, 128, 1, 4, 6, 64>(epi, p, ks, s);
-    return launch_lds_tile<32, 128, 1, 4, 6, 64>(epi, p, s);
+    while (ks < 16 && tiles * ks * 2 <= 4 * cus && KT / (ks * 2) >= 8 && fits(ks * 2)) ks *= 2;
+    return launch_tile_index(9, epi, p, ks, s);
   }
   // Long K with a few hundred rows (the down projection of 512 rows): 256 x 128
   // tiles with K split four ways re-read the activations and weights half as
   // often as the 128 x 64 tiles, at the same workgroup count.
-  constexpr TileShape kLongK{256, 128, 4, 2, 64};
-  if (p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kLongK) && p.part &&
-      (size_t)4 * p.M * p.N * sizeof(float) <= p.part_bytes)
-    return launch_split<256, 128, 4, 2, 3, 64>(epi, p, 4, s);
+  if (p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[2]) && fits(4))
+    return launch_tile_index(2, epi, p, 4, s);
   // 33..256 rows, epilogues other than SwiGLU (o, down, the fusion products):
   // the weights stream with few tiles, so 128 x 64 tiles with K split until
-  // the grid has 256 workgroups (9B-shaped down on 128 rows: 48 us against 70;
-  // o on 256 rows of the 27B shape: 58 us against 71).  SwiGLU keeps its wide
-  // tiles, which measured faster there.
-  constexpr TileShape kMid{128, 64, 4, 2, 64};
-  if (epi != kEpiSwiglu && p.M > 32 && p.M <= 256 && tile_ok(p, epi, kMid) && p.part) {
+  // the grid has a workgroup per compute unit (9B-shaped down on 128 rows:
+  // 48 us against 70; o on 256 rows of the 27B shape: 58 us against 71).
+  // SwiGLU keeps its wide tiles, which measured faster there.
+  if (epi != kEpiSwiglu && p.M > 32 && p.M <= 256 && tile_ok(p, epi, kTiles[3]) && p.part) {
     const long tiles = (long)((p.M + 127) / 128) * (p.N / 64);
     int ks = 2;
-    while (ks < 8 && tiles * ks < 256) ks *= 2;
-    if (p.K / 64 / ks >= 8 && (size_t)ks * p.M * p.N * sizeof(float) <= p.part_bytes)
-      return launch_split<128, 64, 4, 2, 6, 64>(epi, p, ks, s);
+    while (ks < 8 && tiles * ks < cus) ks *= 2;
+    if (p.K / 64 / ks >= 8 && fits(ks)) return launch_tile_index(3, epi, p, ks, s);
   }
   // First tile (in preference order) that gives at least one workgroup per
-  // compute unit (256), else the valid tile with the most workgroups.
+  // compute unit, else the valid tile with the most workgroups.
   const int* order = epi == kEpiSwiglu ? kOrderSwiglu : kOrderResid;
   int best = -1;
   long best_tiles = -1;
-  for (int i = 0; i < kNumTiles; ++i) {
+  for (int i = 0; i < 9; ++i) {
     const int c = order[i];
     if (!tile_ok(p, epi, kTiles[c])) continue;
     const long tiles = (long)((p.M + kTiles[c].bm - 1) / kTiles[c].bm) * (p.N / kTiles[c].bn);
-    if (tiles >= 256) { best = c; break; }
+    if (tiles >= cus) { best = c; break; }
     if (tiles > best_tiles) { best_tiles = tiles; best = c; }
   }
-  switch (best) {
-    case 0: return launch_lds_tile<256, 256, 2, 4, 3, 32>(epi, p, s);
-    case 1: return launch_lds_tile<256, 192, 4, 2, 3, 32>(epi, p, s);
-    case 2: return launch_lds_tile<256, 128, 4, 2, 3, 64>(epi, p, s);
-    case 3: return launch_lds_tile<128, 64, 4, 2, 6, 64>(epi, p, s);
-    case 4: return launch_lds_tile<64, 64, 2, 2, 8, 64>(epi, p, s);
-    case 5: return launch_lds_tile<32, 64, 1, 2, 8, 64>(epi, p, s);
-    case 6: return launch_lds_tile<16, 32, 1, 1, 8, 64>(epi, p, s);
-    case 7: return launch_lds_tile<16, 16, 1, 1, 8, 64>(epi, p, s);
-    case 8: return launch_lds_tile<16, 32, 1, 1, 8, 32>(epi, p, s);
-  }
-  return hipErrorInvalidValue;
+  return launch_tile_index(best, epi, p, 1, s);
 }
 
 }  // namespace sp

@@ -9,13 +9,20 @@ namespace sp {
 // Storage types; bf16-storage configs compute with fp16 activations (kF16).
 enum DType { kF32 = 0, kBF16 = 1, kF16 = 2 };
 
+// Bits of the status word a forward's kernels set (atomic OR) on conditions the
+// host cannot see: a seq_len outside [0, max_seq_len] (the kernels clamp it),
+// and an fp16 activation that left fp16's range (stored as inf).
+enum StatusBits { kStatusSeqLen = 16, kStatusRange = 32 };
+
 // ---------------------------------------------------------------- soft-row prep
 // out[r][i] = x[r][i] / sqrt(mean_i x[r][i]^2 + eps) * gain[i], rows r < rows
 // (row strides ld_x, ld_out in elements).  gain2 (nullable): the result is
 // normed once more with gain2 (RMSNorm(RMSNorm(x; gain); gain2)), in fp32.
+// status (nullable): kStatusRange is set if an fp16 output exceeds fp16's range.
 hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const void* x,
                                int64_t ld_x, const void* gain, const void* gain2, void* out,
-                               int64_t ld_out, int rows, int d, float eps, hipStream_t s);
+                               int64_t ld_out, int rows, int d, float eps, int* status,
+                               hipStream_t s);
 
 // Soft rows j = 0..k-1 of a launch belong to tasks of k_task rows each (one-pass:
 // every task's soft prompt; recursive: k = k_task = 1).  Row j of its task
@@ -26,6 +33,7 @@ struct RopeParams {
   const float* qkv;        // [k][(n_q + 2 n_kv) hd] fp32 ([B][k][...] when per_seq)
   const int* seq_lens;     // device [B]
   const int* err;          // nullable: skip everything if *err != 0
+  int* status;             // kStatusSeqLen for a seq_len outside [0, max_seq_len]
   void* q;                 // [B][n_kv][r_alloc][hd], scaled by q_scale
   void* k_soft;            // [B][n_kv][ks][hd] (rotated soft keys)
   void* v_soft;            // [n_kv][ks][hd] (batch-invariant), or [B][n_kv][ks][hd] (per_seq)
@@ -64,6 +72,7 @@ struct AttnParams {
   float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
   int n_kv, rows, r_alloc, n_qgroups;
   int bs_log2, mbps, max_seq_len, split_len, max_splits;
+  int num_cus;             // compute units of the device
 };
 // Workgroups of the bf16 attention kernel one compute unit holds: three by LDS,
 // and at most 12 waves (head_dim 128) or 20 (64) by VGPRs.
@@ -91,6 +100,8 @@ struct MergeParams {
   const void* v_soft;
   const void* v_soft_lo;
   void* out;               // [B out_rows][n_q hd] (activation dtype)
+  int* status;             // kStatusRange if an fp16 output exceeds fp16's range
+  int min_wgs;             // fewest workgroups the soft-row blocking may leave (4 per compute unit)
   int n_kv, group, rows, r_alloc, hd, ks, max_splits, split_len, max_seq_len, n_q;
   // Row r holds query qi = r / group of its sequence: soft row
   // j = (qi / q_per_task) * k_task + q_first + qi % q_per_task + step, which
@@ -124,9 +135,19 @@ struct GemmParams {
   // launcher splits K only when the partials fit in part_bytes
   float* part;
   size_t part_bytes;
+  int* status;             // kStatusRange if an fp16 SwiGLU output exceeds fp16's range
+  int b_f16;               // the weight blocks are fp16 (a converted image), not bf16
+  int n_cus, n_xcd;        // compute units and XCDs of the device
+  int group_m;             // row tiles per group of the tile order (0: the launcher's choice)
 };
 // dt: storage dtype of the weights (kF32: fp32 VALU path; kBF16: fp16 MFMA path)
 hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p, hipStream_t s);
+// One tile shape of the fp16 MFMA path (index into the tile table of gemm.hip),
+// K split ksplit ways: for measurement; launch_gemm chooses for the forward.
+hipError_t launch_gemm_tile(Epilogue epi, const GemmParams& p, int tile, int ksplit, hipStream_t s);
+// Sum of ksplit fp32 partial slices in p.part and the epilogue (tile width bn,
+// for the SwiGLU column interleave).
+hipError_t launch_gemm_reduce(Epilogue epi, const GemmParams& p, int ksplit, int bn, hipStream_t s);
 
 // ---------------------------------------------------------------- read-out
 struct ClsParams {
@@ -154,5 +175,19 @@ struct ValidateParams {
   int64_t cls_vocab;
 };
 hipError_t launch_validate(const ValidateParams& p, int batch, hipStream_t s);
+
+// ---------------------------------------------------------------- workspace guards, weight image
+// Fill n 32-bit words at p with `value` (a kernel, so it may be captured in a graph).
+hipError_t launch_fill_words(uint32_t* p, size_t n, uint32_t value, hipStream_t s);
+// Check n_guards guard areas of `words` 32-bit words each, at byte offsets
+// offs[i] (device array) from base, against `value`; *flag |= bit on a mismatch.
+hipError_t launch_check_guards(const char* base, const uint64_t* offs, int n_guards, int words,
+                               uint32_t value, int* flag, int bit, hipStream_t s);
+// fp16 copy of n bf16 values (exact for magnitudes in fp16's normal range; the
+// same conversion the projections apply to bf16 weights per fragment).
+hipError_t launch_bf16_to_f16(const void* src, void* dst, size_t n, hipStream_t s);
+// Compare the n_words header words at image against expect (device); *flag |= bit on a mismatch.
+hipError_t launch_check_header(const uint32_t* image, const uint32_t* expect, int n_words, int* flag,
+                               int bit, hipStream_t s);
 
 }  // namespace sp

@@ -88,6 +88,7 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   };
   RowIn cur;
   if (wave < nrows) load_row(wave, cur);
+  bool oor = false;
 
   // stage the keys and values of the workgroup's window
   const int64_t ko = (((int64_t)b * p.n_kv + g) * p.ks + j_lo) * HD;                      // [ks][hd]
@@ -184,8 +185,15 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
     TO* out = (TO*)p.out + ((int64_t)b * p.out_rows + p.out_off + qi) * ((int64_t)p.n_q * HD) +
               (int64_t)h * HD + i0;
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) out[d] = from_f32<TO>(acc[d] * inv);
+    for (int d = 0; d < DPL; ++d) {
+      out[d] = from_f32<TO>(acc[d] * inv);
+      if constexpr (sizeof(TO) == 2) oor |= !(fabsf(acc[d] * inv) <= 65504.0f);
+    }
   }
+  // an fp16 output out of fp16's range (a convex combination of the values,
+  // so only values out of range can cause it)
+  if constexpr (sizeof(TO) == 2)
+    if (__any(oor) && lane == 0 && p.status) atomicOr(p.status, kStatusRange);
 }
 
 }  // namespace
@@ -197,15 +205,17 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
   if (nk_max > 64 || p.rows % p.group) return hipErrorInvalidValue;
   if (p.q_per_task < 1 || (p.rows / p.group) % p.q_per_task) return hipErrorInvalidValue;
   const int tasks = p.rows / p.group / p.q_per_task;
-  // Soft rows per workgroup: the most (a power of two) that still leave 1024
-  // workgroups (4 per compute unit).  Each workgroup stages its key window once
-  // and then streams its rows' partials; measured against 256-4096 workgroups
-  // this was fastest on every workload (long context: 32 us against 44 us at
-  // one soft row per workgroup; 27B shape: 0.37 ms against 0.86 ms).
+  // Soft rows per workgroup: the most (a power of two) that still leave
+  // min_wgs workgroups (4 per compute unit).  Each workgroup stages its key
+  // window once and then streams its rows' partials; measured against 1-16
+  // workgroups per compute unit this was fastest on every workload (long
+  // context: 32 us against 44 us at one soft row per workgroup; 27B shape:
+  // 0.37 ms against 0.86 ms).
   MergeParams q = p;
+  const int64_t min_wgs = p.min_wgs > 0 ? p.min_wgs : 1024;
   q.rw = 1;
   while (2 * q.rw <= p.q_per_task &&
-         (int64_t)batch * p.n_kv * tasks * ((p.q_per_task + 2 * q.rw - 1) / (2 * q.rw)) >= 1024)
+         (int64_t)batch * p.n_kv * tasks * ((p.q_per_task + 2 * q.rw - 1) / (2 * q.rw)) >= min_wgs)
     q.rw *= 2;
   const int bpt = (p.q_per_task + q.rw - 1) / q.rw;
   const dim3 grid(tasks * bpt, p.n_kv, batch);

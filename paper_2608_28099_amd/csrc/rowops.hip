@@ -1,6 +1,8 @@
 // Row kernels of the probe forward: RMSNorm, RoPE at positions N_b + j with the
 // scatter into the attention layouts, final norm + read-out + linear
 // classifier, and the debug validation of device-resident metadata.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -37,10 +39,16 @@ __device__ __forceinline__ void store4(T* p, const float (&v)[4]) {
   }
 }
 
+// Sets kStatusRange in *status (nullable) when an fp16 output leaves fp16's
+// range (it is then stored as inf).
+__device__ __forceinline__ void flag_range(bool out_of_range, int* status) {
+  if (__any(out_of_range) && (threadIdx.x & 63) == 0 && status) atomicOr(status, kStatusRange);
+}
+
 template <typename TI, typename TG, typename TO>
 __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, const TG* gain,
                                                     const TG* gain2, TO* out, int64_t ld_out, int d,
-                                                    float eps) {
+                                                    float eps, int* status) {
   __shared__ float red[4];
   const int r = blockIdx.x;
   const TI* xr = x + (int64_t)r * ld_x;
@@ -80,11 +88,18 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, c
     }
   }
   TO* orow = out + (int64_t)r * ld_out;
+  bool oor = false;
 #pragma unroll
   for (int c = 0; c < kRowChunks; ++c) {
     const int i = 4 * (threadIdx.x + 256 * c);
-    if (i < d) store4(orow + i, v[c]);
+    if (i < d) {
+      store4(orow + i, v[c]);
+      if constexpr (sizeof(TO) == 2)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) oor |= !(fabsf(v[c][e]) <= 65504.0f);
+    }
   }
+  if constexpr (sizeof(TO) == 2) flag_range(oor, status);
 }
 
 // ---------------------------------------------------------------- RoPE + scatter
@@ -111,6 +126,10 @@ __global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
   if (p.err && *p.err) return;
   const int hd = p.hd, half = hd / 2;
   int n = p.seq_lens[b];
+  // a length outside [0, max_seq_len] is clamped (every kernel does the same)
+  // and reported through the status word
+  if ((n < 0 || n > p.max_seq_len) && j == 0 && threadIdx.x == 0 && p.status)
+    atomicOr(p.status, kStatusSeqLen);
   n = n < 0 ? 0 : (n > p.max_seq_len ? p.max_seq_len : n);
   const int jj = j % p.k_task;
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
@@ -251,23 +270,80 @@ __global__ void validate_meta(const ValidateParams p) {
   }
 }
 
+// ---------------------------------------------------------------- workspace guards, weight image
+__global__ void fill_words(uint32_t* p, size_t n, uint32_t value) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = value;
+}
+
+// One workgroup per guard area.
+__global__ void check_guards(const char* base, const uint64_t* offs, int words, uint32_t value, int* flag,
+                             int bit) {
+  const uint32_t* g = reinterpret_cast<const uint32_t*>(base + offs[blockIdx.x]);
+  bool bad = false;
+  for (int i = threadIdx.x; i < words; i += blockDim.x) bad |= g[i] != value;
+  if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(flag, bit);
+}
+
+__global__ void bf16_to_f16(const uint32_t* src, uint32_t* dst, size_t n2) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n2; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = bf16x2_to_f16x2(src[i]);
+}
+
+__global__ void check_header(const uint32_t* image, const uint32_t* expect, int n_words, int* flag, int bit) {
+  const int i = threadIdx.x;
+  const bool bad = i < n_words && image[i] != expect[i];
+  if (__any(bad) && i == 0) atomicOr(flag, bit);
+}
+
 }  // namespace
+
+hipError_t launch_fill_words(uint32_t* p, size_t n, uint32_t value, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const size_t blocks = std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(fill_words, dim3((unsigned)blocks), dim3(256), 0, s, p, n, value);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_guards(const char* base, const uint64_t* offs, int n_guards, int words,
+                               uint32_t value, int* flag, int bit, hipStream_t s) {
+  if (n_guards <= 0) return hipSuccess;
+  hipLaunchKernelGGL(check_guards, dim3(n_guards), dim3(64), 0, s, base, offs, words, value, flag, bit);
+  return hipGetLastError();
+}
+
+hipError_t launch_bf16_to_f16(const void* src, void* dst, size_t n, hipStream_t s) {
+  if (n % 2) return hipErrorInvalidValue;
+  if (n == 0) return hipSuccess;
+  const size_t blocks = std::min<size_t>((n / 2 + 255) / 256, 8192);
+  hipLaunchKernelGGL(bf16_to_f16, dim3((unsigned)blocks), dim3(256), 0, s, (const uint32_t*)src,
+                     (uint32_t*)dst, n / 2);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_header(const uint32_t* image, const uint32_t* expect, int n_words, int* flag,
+                               int bit, hipStream_t s) {
+  if (n_words > 64) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(check_header, dim3(1), dim3(64), 0, s, image, expect, n_words, flag, bit);
+  return hipGetLastError();
+}
 
 hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const void* x,
                                int64_t ld_x, const void* gain, const void* gain2, void* out,
-                               int64_t ld_out, int rows, int d, float eps, hipStream_t s) {
+                               int64_t ld_out, int rows, int d, float eps, int* status,
+                               hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (d % 4 || d > 1024 * kRowChunks || ld_x % 4 || ld_out % 4) return hipErrorInvalidValue;
   const dim3 grid(rows), block(256);
   if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
     hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, ld_x,
-                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps);
+                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
   else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kF16)
     hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16>), grid, block, 0, s, (const float*)x, ld_x,
-                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps);
+                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
   else if (in_dt == kF32 && gain_dt == kF32 && out_dt == kF32)
     hipLaunchKernelGGL((rmsnorm_rows<float, float, float>), grid, block, 0, s, (const float*)x, ld_x,
-                       (const float*)gain, (const float*)gain2, (float*)out, ld_out, d, eps);
+                       (const float*)gain, (const float*)gain2, (float*)out, ld_out, d, eps, status);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -136,3 +136,70 @@ def test_bench_refuses_more_than_one_gpu():
                          capture_output=True, text=True, timeout=120)
     assert res.returncode == 2
     assert "one GPU" in res.stderr and not res.stdout.strip()
+
+
+def _split_rule(n_max, batch, n_kv, groups, waves, cus, hd=128):
+    """The documented split rule, restated: splits sized so that the grid at the
+    full batch and length fills one round of resident workgroups (cus x the
+    workgroups a compute unit holds), capped at a third of the longest sequence,
+    rounded up to 256 tokens, at least 1024."""
+    per_cu = min(3, (12 if hd == 128 else 20) // waves)
+    slots = cus * max(per_cu, 1)
+    want = -(-(n_max * batch * n_kv * groups) // slots)
+    third = (n_max + 2) // 3
+    return max(1024, -(-min(want, third) // 256) * 256)
+
+
+@pytest.mark.parametrize("cus", [64, 128, 256, 304, 512])
+def test_split_plan_follows_the_compute_unit_count(cus):
+    """The host plan reads the compute-unit count (a small batch of the long
+    context: the one-round rule binds, not the third-of-a-sequence cap)."""
+    w = configs.WORKLOADS["long_9b_bf16"]
+    cfg = binding.make_config(w, max_batch=4)
+    plan = binding.sp_probe_plan_config(cfg, cus)
+    rows = w.k * w.n_q_heads // w.n_kv_heads
+    assert plan["rows_per_kv_head"] == rows and plan["query_groups"] == 1
+    sl = _split_rule(w.max_seq_len(), 4, w.n_kv_heads, 1, 4, cus)
+    assert plan["split_len"] == sl
+    assert plan["max_splits"] == -(-w.max_seq_len() // sl)
+
+
+def test_split_plan_differs_across_compute_unit_counts_and_matches_workspace_bytes():
+    w = configs.WORKLOADS["long_9b_bf16"]
+    cfg = binding.make_config(w, max_batch=4)
+    a, b = binding.sp_probe_plan_config(cfg, 128), binding.sp_probe_plan_config(cfg, 256)
+    assert a["split_len"] > b["split_len"]   # half the compute units: longer splits
+    assert a["max_splits"] < b["max_splits"]
+    # more splits, more partials in the workspace
+    assert b["workspace_bytes"] > a["workspace_bytes"]
+    # with no device the sizing assumes 256 compute units
+    assert binding.sp_probe_workspace_bytes(cfg) == b["workspace_bytes"]
+
+
+def test_plan_config_rejects_bad_arguments():
+    w = configs.SMALL_BF16
+    cfg = binding.make_config(w)
+    lib = binding.load()
+    z = ctypes.c_int32()
+    assert lib.sp_probe_plan_config(ctypes.byref(cfg), 0, None, None, None, None, None) == -1
+    assert lib.sp_probe_plan_config(ctypes.byref(cfg), 1 << 20, None, None, None, None, None) == -1
+    assert lib.sp_probe_plan_config(None, 256, ctypes.byref(z), None, None, None, None) == -1
+    cfg.head_dim = 96
+    assert lib.sp_probe_plan_config(ctypes.byref(cfg), 256, None, None, None, None, None) == -2
+
+
+def test_packed_image_size():
+    """The fp16 image holds a 256-byte header and the seven matrices, each
+    segment rounded up to 256 bytes; none for fp32 configs."""
+    w = configs.WORKLOADS["9b_bf16"]
+    cfg = binding.make_config(w)
+    d, hd, I = w.hidden, w.head_dim, w.intermediate
+    segs = [(w.n_q_heads + 2 * w.n_kv_heads) * hd * d, d * w.n_q_heads * hd, I * d, I * d, d * I]
+    assert binding.sp_probe_packed_bytes(cfg) == 256 + sum(-(-2 * n // 256) * 256 for n in segs)
+    assert binding.sp_probe_packed_bytes(binding.make_config(configs.TINY_F32)) == 0
+    lib = binding.load()
+    wt = binding.sp_probe_weights()
+    # host checks before any device is needed
+    assert lib.sp_probe_pack_weights(ctypes.byref(binding.make_config(configs.TINY_F32)), ctypes.byref(wt),
+                                     None, 0, None) == -2
+    assert lib.sp_probe_pack_weights(ctypes.byref(cfg), ctypes.byref(wt), None, 0, None) == -1

@@ -35,11 +35,20 @@ def test_bench_prints_the_contract_line(args):
         assert key in d, key
     assert d["n_gpus"] == 1 and d["steps"] == 3 and d["warmup"] == 1
     assert d["value"] > 0 and d["ms_per_step"] > 0 and d["higher_is_better"] is True
-    assert d["dtype"] == "bf16" and isinstance(d["config"], dict) and "workload" in d["config"]
+    assert d["dtype"].startswith("bf16 storage") and isinstance(d["config"], dict) and "workload" in d["config"]
+    assert d["config"]["weights"] == "fp16 image"
+    dist = d["step_time_distribution"]
+    assert dist["steps"] >= 50 and 0 < dist["p10_ms"] <= dist["median_ms"] <= dist["p90_ms"]
     r = d["roofline"]
     for key in ("bound", "achieved", "peak", "unit", "frac", "traffic"):
         assert key in r, key
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000
     assert r["frac"] > 0 and r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-4)
+    assert r["measured_read_peak_gbps"] > 0
+    assert r["frac_of_measured_read_peak"] == pytest.approx(r["achieved"] / r["measured_read_peak_gbps"], abs=1e-3)
+    # the attention stage (split + merge) takes longer than the split kernel alone
+    assert r["mean_launch_ms"] >= r["split_kernel_only"]["mean_launch_ms"]
+    # a KV cache this small is rotated over copies exceeding 1 GB
+    assert d["config"]["kv_copies_rotated"] >= 2
     c = d["cpu_baseline"]
     assert c["kind"] == "oracle" and c["value"] > 0 and c["cores"] >= 1 and c["sample"]

@@ -331,8 +331,16 @@ def test_full_size_every_sequence(w, dev):
     params = inputs.params(w, dev)
     probe = binding.Probe(w)
     announce(f"[full] {w.name}: plan {probe.plan(w.batch)}")
-    got = probe.forward(kv, params).cpu().numpy()
+    # the benchmark's launch configuration reads the fp16 weight image; the
+    # forward without it returns the same logits bit for bit
+    img = binding.pack_weights(w, params)
+    got_t = probe.forward(kv, dict(params, packed=img)).clone()
+    plain = probe.forward(kv, params).clone()
     torch.cuda.synchronize()
+    assert torch.equal(got_t, plain)
+    assert probe.check_device_error() == 0
+    got = got_t.cpu().numpy()
+    del img, plain
     announce(f"[full] {w.name}: forward done")
     assert np.all(np.isfinite(got))
     n = w.batch
