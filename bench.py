@@ -214,9 +214,10 @@ def main():
     run_params = dict(params)
     if w.dtype == "bf16":
         run_params["packed"] = binding.pack_weights(w, params, max_tasks=T)
-    # KV copies so that the cache rotated through exceeds ROTATE_BELOW bytes
-    pool_bytes = kv.pool.numel() * kv.pool.element_size()
-    n_rot = 1 if pool_bytes >= ROTATE_BELOW else min(64, -(-ROTATE_BELOW // pool_bytes) + 1)
+    # KV copies so that the KV the steps read, rotated, exceeds ROTATE_BELOW bytes
+    esz = 2 if w.dtype == "bf16" else 4
+    kv_bytes = int(lens.astype("int64").sum()) * w.n_kv_heads * w.head_dim * 2 * esz
+    n_rot = 1 if kv_bytes >= ROTATE_BELOW else min(64, -(-ROTATE_BELOW // max(kv_bytes, 1)) + 1)
     kvs = [kv] + [inputs.KVCache(kv.pool.clone(), kv.block_table, kv.seq_lens, kv.block_size,
                                  kv.max_blocks_per_seq, kv.n_kv, kv.head_dim) for _ in range(n_rot - 1)]
     plain = binding.Probe(w, split_len=args.split_len, flags=flags, max_tasks=T)
@@ -273,8 +274,6 @@ def main():
     stages, n_fwd = prof.profile_read()   # the event pool keeps the last forwards that fit (all of them here)
     assert 0 < n_fwd <= args.steps
 
-    esz = 2 if w.dtype == "bf16" else 4
-    kv_bytes = int(lens.astype("int64").sum()) * w.n_kv_heads * w.head_dim * 2 * esz
     launches = w.k if recursive else 1   # attention launches per step
     attn_ms = stages["attention"] / (n_fwd * launches)
     stage_ms = (stages["attention"] + stages["merge"]) / (n_fwd * launches)

@@ -81,29 +81,38 @@ def _normal(shape, mean, std, dtype, device, gen) -> torch.Tensor:
     return t
 
 
-def params(w: Workload, device="cpu") -> dict:
+def params(w: Workload, device="cpu", only=None) -> dict:
     """Frozen head weights ([out, in] row-major), norm gains, soft prompts and the
-    linear classifier, in the workload's storage dtype (classifier bias: fp32)."""
+    linear classifier, in the workload's storage dtype (classifier bias: fp32).
+    only: names to draw (each tensor has its own stream, so a subset has the
+    same bytes as in the full set); default all."""
     dt = TORCH_DTYPE[w.dtype]
     d, hd, I = w.hidden, w.head_dim, w.intermediate
     qd, kvd = w.n_q_heads * hd, w.n_kv_heads * hd
     ws, gs = w.weight_std, w.gain_std
-    p = {
-        "soft_prompt": _normal((w.k, d), 0.0, w.soft_std, dt, device, _gen(w, "soft", device)),
-        "in_norm": _normal((d,), 1.0, gs, dt, device, _gen(w, "in_norm", device)),
-        "w_q": _normal((qd, d), 0.0, ws, dt, device, _gen(w, "w_q", device)),
-        "w_k": _normal((kvd, d), 0.0, ws, dt, device, _gen(w, "w_k", device)),
-        "w_v": _normal((kvd, d), 0.0, ws, dt, device, _gen(w, "w_v", device)),
-        "w_o": _normal((d, qd), 0.0, ws, dt, device, _gen(w, "w_o", device)),
-        "post_norm": _normal((d,), 1.0, gs, dt, device, _gen(w, "post_norm", device)),
-        "w_gate": _normal((I, d), 0.0, ws, dt, device, _gen(w, "w_gate", device)),
-        "w_up": _normal((I, d), 0.0, ws, dt, device, _gen(w, "w_up", device)),
-        "w_down": _normal((d, I), 0.0, ws, dt, device, _gen(w, "w_down", device)),
-        "final_norm": _normal((d,), 1.0, gs, dt, device, _gen(w, "final_norm", device)),
-        "w_cls": _normal((w.n_classes, d), 0.0, ws, dt, device, _gen(w, "w_cls", device)),
-        "b_cls": (_normal((w.n_classes,), 0.0, 1.0, torch.float32, device, _gen(w, "b_cls", device))
-                  if w.cls_bias else None),
+    spec = {
+        "soft_prompt": ((w.k, d), 0.0, w.soft_std, dt, "soft"),
+        "in_norm": ((d,), 1.0, gs, dt, "in_norm"),
+        "w_q": ((qd, d), 0.0, ws, dt, "w_q"),
+        "w_k": ((kvd, d), 0.0, ws, dt, "w_k"),
+        "w_v": ((kvd, d), 0.0, ws, dt, "w_v"),
+        "w_o": ((d, qd), 0.0, ws, dt, "w_o"),
+        "post_norm": ((d,), 1.0, gs, dt, "post_norm"),
+        "w_gate": ((I, d), 0.0, ws, dt, "w_gate"),
+        "w_up": ((I, d), 0.0, ws, dt, "w_up"),
+        "w_down": ((d, I), 0.0, ws, dt, "w_down"),
+        "final_norm": ((d,), 1.0, gs, dt, "final_norm"),
+        "w_cls": ((w.n_classes, d), 0.0, ws, dt, "w_cls"),
+        "b_cls": ((w.n_classes,), 0.0, 1.0, torch.float32, "b_cls"),
     }
+    p = {}
+    for name, (shape, mean, std, tdt, tag) in spec.items():
+        if only is not None and name not in only:
+            continue
+        if name == "b_cls" and not w.cls_bias:
+            p[name] = None
+            continue
+        p[name] = _normal(shape, mean, std, tdt, device, _gen(w, tag, device))
     return p
 
 
