@@ -269,6 +269,24 @@ int sp_probe_forward_multi(sp_probe_t* h, const sp_kv_cache* kv_cache, const int
                            const int32_t* block_table, int32_t n_tasks, const void* soft_prompts,
                            const sp_probe_weights* weights, float* logits, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): sp_probe_forward
+ * without a handle.  The workspace is a static device array of 64 MiB per
+ * device (allocated when the library's code object loads, held until the
+ * process ends); the call allocates nothing, host or device.  cfg is checked
+ * as by sp_probe_init; every other argument, the checks and the results are
+ * those of sp_probe_forward (the same kernels and plan: logits identical bit
+ * for bit to a handle's).  Errors: SP_ERR_CAPACITY if the config's workspace
+ * (sp_probe_plan_config) exceeds 64 MiB; SP_ERR_UNSUPPORTED for SP_FLAG_DEBUG
+ * or SP_FLAG_PROFILE (no handle holds their flags or events; the status word
+ * is not reported either).  All calls on one device share its array and the
+ * last call's contents stay in it: calls that overlap on one device (other
+ * streams, other threads) race and must be ordered by the caller.  The first
+ * call on a device resolves the array's address there. */
+int sp_probe_forward_noalloc(const sp_probe_config* cfg, const sp_kv_cache* kv_cache, const int32_t* seq_lens,
+                             const int32_t* block_table, const void* soft_prompt,
+                             const sp_probe_weights* weights, float* logits, void* stream);
+
 /* Free the workspace and the handle (waits for the device). NULL is accepted. */
 int sp_probe_destroy(sp_probe_t* h);
 

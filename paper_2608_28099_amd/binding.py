@@ -30,7 +30,8 @@ EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward",
            "sp_probe_forward_multi", "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
            "sp_probe_tap_bytes", "sp_probe_copy_tap", "sp_probe_check_device_error",
            "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive", "sp_probe_plan_config",
-           "sp_probe_packed_bytes", "sp_probe_pack_weights", "sp_probe_measure_read")
+           "sp_probe_packed_bytes", "sp_probe_pack_weights", "sp_probe_measure_read",
+           "sp_probe_forward_noalloc")
 
 
 class sp_probe_config(ctypes.Structure):
@@ -85,6 +86,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_init.restype = ctypes.c_int
     lib.sp_probe_forward.argtypes = [vp, P(sp_kv_cache), vp, vp, vp, P(sp_probe_weights), vp, vp]
     lib.sp_probe_forward.restype = ctypes.c_int
+    lib.sp_probe_forward_noalloc.argtypes = [P(sp_probe_config), P(sp_kv_cache), vp, vp, vp, P(sp_probe_weights),
+                                             vp, vp]
+    lib.sp_probe_forward_noalloc.restype = ctypes.c_int
     lib.sp_probe_forward_multi.argtypes = [vp, P(sp_kv_cache), vp, vp, ctypes.c_int32, vp,
                                            P(sp_probe_weights), vp, vp]
     lib.sp_probe_forward_multi.restype = ctypes.c_int
@@ -151,6 +155,12 @@ def sp_probe_forward(h, kv: sp_kv_cache, seq_lens, block_table, soft_prompt,
                      weights: sp_probe_weights, logits, stream) -> int:
     return load().sp_probe_forward(h, ctypes.byref(kv), seq_lens, block_table, soft_prompt,
                                    ctypes.byref(weights), logits, stream)
+
+
+def sp_probe_forward_noalloc(cfg: sp_probe_config, kv: sp_kv_cache, seq_lens, block_table, soft_prompt,
+                             weights: sp_probe_weights, logits, stream) -> int:
+    return load().sp_probe_forward_noalloc(ctypes.byref(cfg), ctypes.byref(kv), seq_lens, block_table, soft_prompt,
+                                           ctypes.byref(weights), logits, stream)
 
 
 def sp_probe_forward_multi(h, kv: sp_kv_cache, seq_lens, block_table, n_tasks: int, soft_prompts,

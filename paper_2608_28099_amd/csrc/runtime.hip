@@ -7,6 +7,8 @@
 #include <cstdint>
 #include <cstring>
 #include <deque>
+#include <functional>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -514,7 +516,7 @@ SP_API const char* sp_probe_status_string(int status) {
     case SP_ERR_NO_DEVICE: return "SP_ERR_NO_DEVICE: no gfx950 HIP device";
     case SP_ERR_OUT_OF_MEMORY: return "SP_ERR_OUT_OF_MEMORY: workspace allocation failed";
     case SP_ERR_HIP: return "SP_ERR_HIP: HIP runtime or launch error";
-    case SP_ERR_CAPACITY: return "SP_ERR_CAPACITY: batch exceeds max_batch";
+    case SP_ERR_CAPACITY: return "SP_ERR_CAPACITY: batch exceeds max_batch, or the workspace exceeds the static scratch";
     case SP_ERR_DEVICE_DATA: return "SP_ERR_DEVICE_DATA: invalid seq_lens, block ids, class rows or weight image on the device";
     case SP_ERR_RANGE: return "SP_ERR_RANGE: an fp16 activation exceeded fp16's range";
     case SP_ERR_INTERNAL: return "SP_ERR_INTERNAL: a workspace guard word was overwritten";
@@ -1092,4 +1094,77 @@ SP_API int sp_probe_profile_read(sp_probe_t* h, float* stage_ms, int32_t n_stage
   h->records.clear();
   h->cursor = 0;
   return SP_OK;
+}
+
+// ---------------------------------------------------------------- forward without allocation
+// For callers that cannot allocate (code under graph capture, serving loops,
+// harnesses that forbid hipMalloc): the workspace is a file-scope device array
+// of kScratchBytes, one per device the library runs on, held until the process
+// ends.  Host code must use its device address from hipGetSymbolAddress, taken
+// once per device with that device current; the array's name is not a device
+// address on the host.
+namespace {
+
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+struct ScratchDev {
+  std::once_flag once;
+  int status;   // SP_OK once set up
+  char* ptr;    // device address of this device's scratch array
+  int num_cus, n_xcd;
+};
+ScratchDev g_scratch[kMaxDevices];
+
+void setup_scratch(ScratchDev& sd) {
+  int cus = 0, xcd = 0;
+  sd.status = check_device(&cus, &xcd);
+  if (sd.status != SP_OK) return;
+  void* p = nullptr;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+    sd.status = SP_ERR_HIP;
+    return;
+  }
+  sd.ptr = static_cast<char*>(p);
+  sd.num_cus = cus;
+  sd.n_xcd = xcd;
+}
+
+}  // namespace
+
+SP_API int sp_probe_forward_noalloc(const sp_probe_config* cfg, const sp_kv_cache* kv, const int32_t* seq_lens,
+                                    const int32_t* block_table, const void* soft_prompt,
+                                    const sp_probe_weights* weights, float* logits, void* stream) {
+  int st = check_config(cfg);
+  if (st != SP_OK) return st;
+  if (cfg->flags & (SP_FLAG_DEBUG | SP_FLAG_PROFILE)) return SP_ERR_UNSUPPORTED;
+  int dev = 0, count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count < 1 || hipGetDevice(&dev) != hipSuccess)
+    return SP_ERR_NO_DEVICE;
+  if (dev < 0 || dev >= kMaxDevices) return SP_ERR_UNSUPPORTED;
+  ScratchDev& sd = g_scratch[dev];
+  std::call_once(sd.once, setup_scratch, std::ref(sd));
+  if (sd.status != SP_OK) return sd.status;
+  const Plan pl = make_plan(*cfg, sd.num_cus);
+  if (pl.total > kScratchBytes) return SP_ERR_CAPACITY;
+  const Ctx x{cfg, &pl, sd.ptr, sd.num_cus, sd.n_xcd, nullptr};
+  // host checks first: on error nothing is enqueued
+  bool noop = false;
+  st = check_forward(*cfg, pl, kv, seq_lens, block_table, soft_prompt, weights, logits, &noop);
+  if (st != SP_OK || noop) return st;
+  // The array keeps the last call's contents (possibly of another config):
+  // clear what a forward expects to start at zero, the padded query rows and
+  // soft key/value slots and the flag words, with a fill kernel.
+  hipStream_t s = (hipStream_t)stream;
+  const size_t zero_from[] = {pl.off_q, pl.off_ksoft, pl.off_vsoft, pl.off_q_lo, pl.off_ksoft_lo,
+                              pl.off_vsoft_lo, pl.off_err};
+  const size_t zero_to[] = {pl.off_ksoft, pl.off_vsoft, pl.off_q_lo, pl.off_ksoft_lo, pl.off_vsoft_lo,
+                            pl.off_opart, pl.off_err + 256};
+  for (int i = 0; i < 7; ++i)
+    if (zero_to[i] > zero_from[i] &&
+        launch_fill_words((uint32_t*)(sd.ptr + zero_from[i]), (zero_to[i] - zero_from[i]) / 4, 0u, s) != hipSuccess)
+      return SP_ERR_HIP;
+  return forward_one_pass(x, kv, seq_lens, block_table, 1, soft_prompt, weights, logits, stream);
 }

@@ -382,7 +382,10 @@ int main(int argc, char** argv) {
     g.where = "no device";
     sp_probe_t* h = nullptr;
     g.expect(sp_probe_init(&fixed[1].cfg, &h) == SP_ERR_NO_DEVICE && h == nullptr, "init without a device");
+    sp_kv_cache kv{};
     sp_probe_weights wt{};
+    g.expect(sp_probe_forward_noalloc(&fixed[1].cfg, &kv, nullptr, nullptr, nullptr, &wt, nullptr, nullptr) ==
+                 SP_ERR_NO_DEVICE, "forward without allocation, no device");
     g.expect(sp_probe_pack_weights(&fixed[1].cfg, &wt, nullptr, 0, nullptr) == SP_ERR_INVALID_ARG, "pack arguments");
   }
   std::printf("host runtime check: %ld checks, %d random configs accepted, %ld failures\n", g.checks, accepted,
