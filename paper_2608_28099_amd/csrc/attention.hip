@@ -43,11 +43,13 @@ __device__ __forceinline__ int64_t phys_block(const AttnParams& p, int b, int t)
 // (log2 units), so probabilities stay below 2^8 between moves.
 constexpr float kRescaleLog2 = 8.0f;
 
-// The wave's running softmax state for its 16 query rows.
-template <int HD>
+// The wave's running softmax state for its 16 query rows.  F16: the fp16
+// variant (single fp16 products on K and V converted to fp16 in LDS).
+template <int HD, bool F16>
 struct RowState {
   static constexpr int NC = HD / 32, NT = HD / 16;
-  bf16x8 qh[NC], ql[NC];  // Q[row li][8 (la*NC + c) .. +7], hi and lo parts
+  bf16x8 qh[NC], ql[NC];  // Q[row li][8 (la*NC + c) .. +7], hi and lo parts (bf16 products)
+  f16x8 q16[NC];          // the same rows rounded to fp16 (fp16 products)
   f32x4 o[NT];            // O[row 4la + r][16nt + li], unnormalised
   float m, l;             // reference max of row li (log2 units); this lane's part of its sum
 };
@@ -59,8 +61,8 @@ struct RowState {
 // first unit of a split (FIRST), whose reference is still the -1e30 start
 // value: it takes the raw scores.  softmax_pv_unit: vf[nt] =
 // V[tokens 8la..8la+7][16nt + li]; keys at or past `limit` are masked.
-template <int HD, bool FIRST>
-__device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&kf)[2][HD / 32],
+template <int HD, bool FIRST, bool F16>
+__device__ __forceinline__ void qk_unit(const RowState<HD, F16>& st, const u32x4 (&kf)[2][HD / 32],
                                         f32x4& s0, f32x4& s1) {
   constexpr int NC = HD / 32;
   const float init = FIRST ? 0.f : -st.m;
@@ -68,10 +70,16 @@ __device__ __forceinline__ void qk_unit(const RowState<HD>& st, const bf16x8 (&k
   s1 = s0;
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    s0 = mfma16x16x32_bf16(kf[0][c], st.qh[c], s0);
-    s1 = mfma16x16x32_bf16(kf[1][c], st.qh[c], s1);
-    s0 = mfma16x16x32_bf16(kf[0][c], st.ql[c], s0);
-    s1 = mfma16x16x32_bf16(kf[1][c], st.ql[c], s1);
+    if constexpr (F16) {
+      s0 = mfma16x16x32(__builtin_bit_cast(f16x8, kf[0][c]), st.q16[c], s0);
+      s1 = mfma16x16x32(__builtin_bit_cast(f16x8, kf[1][c]), st.q16[c], s1);
+    } else {
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, kf[0][c]), k1 = __builtin_bit_cast(bf16x8, kf[1][c]);
+      s0 = mfma16x16x32_bf16(k0, st.qh[c], s0);
+      s1 = mfma16x16x32_bf16(k1, st.qh[c], s1);
+      s0 = mfma16x16x32_bf16(k0, st.ql[c], s0);
+      s1 = mfma16x16x32_bf16(k1, st.ql[c], s1);
+    }
   }
 }
 
@@ -85,9 +93,9 @@ __device__ __forceinline__ void split_pair(float p0, float p1, uint32_t& hi, uin
   lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{p0 - h0, p1 - h1}, bf16x2v));
 }
 
-template <int HD, bool FIRST>
-__device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x4 s1,
-                                                const bf16x8 (&vf)[HD / 16], int la, int limit) {
+template <int HD, bool FIRST, bool F16>
+__device__ __forceinline__ void softmax_pv_unit(RowState<HD, F16>& st, f32x4 s0, f32x4 s1,
+                                                const u32x4 (&vf)[HD / 16], int la, int limit) {
   constexpr int NT = HD / 16;
   // sc = s - m, or s in the first unit
   float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
@@ -142,15 +150,25 @@ __device__ __forceinline__ void softmax_pv_unit(RowState<HD>& st, f32x4 s0, f32x
     ps += pv[i];
   }
   st.l += ps;
-  uint32_t hw[4], lw[4];
+  if constexpr (F16) {
+    // p < 2^8 between reference moves: fp16 (round to nearest even) keeps 11 bits
+    f16x8 p16;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) split_pair(pv[2 * q], pv[2 * q + 1], hw[q], lw[q]);
-  const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
-  const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
+    for (int i = 0; i < 8; ++i) p16[i] = (f16)pv[i];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    st.o[nt] = mfma16x16x32_bf16(ph, vf[nt], st.o[nt]);
-    st.o[nt] = mfma16x16x32_bf16(pl, vf[nt], st.o[nt]);
+    for (int nt = 0; nt < NT; ++nt) st.o[nt] = mfma16x16x32(p16, __builtin_bit_cast(f16x8, vf[nt]), st.o[nt]);
+  } else {
+    uint32_t hw[4], lw[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) split_pair(pv[2 * q], pv[2 * q + 1], hw[q], lw[q]);
+    const bf16x8 ph = __builtin_bit_cast(bf16x8, u32x4{hw[0], hw[1], hw[2], hw[3]});
+    const bf16x8 pl = __builtin_bit_cast(bf16x8, u32x4{lw[0], lw[1], lw[2], lw[3]});
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16x8 v = __builtin_bit_cast(bf16x8, vf[nt]);
+      st.o[nt] = mfma16x16x32_bf16(ph, v, st.o[nt]);
+      st.o[nt] = mfma16x16x32_bf16(pl, v, st.o[nt]);
+    }
   }
 }
 
@@ -218,47 +236,93 @@ __device__ __forceinline__ void zero_tail(u32x4* sb, int limit, int tid) {
   }
 }
 
-// A wave's fragments of a staged unit, then the unit's softmax and products.
-template <int HD, bool FIRST>
-__device__ __forceinline__ void compute_unit(RowState<HD>& st, const u32x4* sb, int limit, int li,
-                                             int la) {
+// Wait until at most k units of PPL loads each remain in flight (k <= K).
+template <int PPL, int K>
+__device__ __forceinline__ void wait_units_le(int k) {
+  if constexpr (K == 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (k >= K) wait_vmcnt<K * PPL>();
+    else wait_units_le<PPL, K - 1>(k);
+  }
+}
+
+// A wave's fragments of a staged unit, then the unit's softmax and products
+// for each of the wave's ntw (<= TPW) query tiles: every K and V fragment read
+// from LDS serves all of them.
+template <int HD, bool FIRST, bool F16, int TPW>
+__device__ __forceinline__ void compute_unit(RowState<HD, F16> (&st)[TPW], int ntw, const u32x4* sb, int limit,
+                                             int li, int la) {
   constexpr int NC = HD / 32, NT = HD / 16;
-  f32x4 s0, s1;
+  f32x4 s0[TPW], s1[TPW];
   {
-    bf16x8 kf[2][NC];
+    u32x4 kf[2][NC];
 #pragma unroll
     for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int c = 0; c < NC; ++c)
-        kf[h][c] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::k_piece(h, la * NC + c, li)]);
-    qk_unit<HD, FIRST>(st, kf, s0, s1);
+      for (int c = 0; c < NC; ++c) kf[h][c] = sb[UnitLayout<HD>::k_piece(h, la * NC + c, li)];
+#pragma unroll
+    for (int t = 0; t < TPW; ++t)
+      if (t < ntw) qk_unit<HD, FIRST, F16>(st[t], kf, s0[t], s1[t]);
   }
   // V fragments are read only once the QK products are issued, into the
   // registers the K fragments held.
   __builtin_amdgcn_sched_barrier(0);
-  bf16x8 vf[NT];
+  u32x4 vf[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
-    vf[nt] = __builtin_bit_cast(bf16x8, sb[UnitLayout<HD>::v_piece(nt, li, la)]);
-  softmax_pv_unit<HD, FIRST>(st, s0, s1, vf, la, limit);
+  for (int nt = 0; nt < NT; ++nt) vf[nt] = sb[UnitLayout<HD>::v_piece(nt, li, la)];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t)
+    if (t < ntw) softmax_pv_unit<HD, FIRST, F16>(st[t], s0[t], s1[t], vf, la, limit);
 }
 
-// W waves per workgroup, one per 16-row query tile.  Three LDS stages: unit u
-// is computed from stage u % 3 while units u + 1 and u + 2 are in flight.
-template <int HD, int W, bool ROT>
+// fp16 variant: convert a landed unit's K and V tiles in LDS from bf16 to fp16
+// in place (exact for magnitudes in fp16's normal range), once for all the
+// workgroup's waves, zeroing V slots at or past `limit` (they may hold NaN).
+template <int HD, int W>
+__device__ __forceinline__ void convert_unit(u32x4* sb, int limit, int tid) {
+  using L = UnitLayout<HD>;
+  for (int q = tid; q < 8 * HD; q += 64 * W) {
+    const bool is_v = q >= 4 * HD;
+    const int piece = is_v ? L::VB + (q - 4 * HD) : (q / (2 * HD)) * L::KHP + q % (2 * HD);
+    u32x4 x = bf16x8_to_f16x8(sb[piece]);
+    if (is_v && limit < 32) {
+      const int qv = q - 4 * HD;
+      const int tk0 = 16 * (qv / (2 * HD)) + 8 * ((qv >> 4) & 1);  // first of the piece's 8 tokens
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const int keep = limit - (tk0 + 2 * w);
+        x[w] &= keep >= 2 ? 0xffffffffu : (keep == 1 ? 0x0000ffffu : 0u);
+      }
+    }
+    sb[piece] = x;
+  }
+}
+
+// W waves per workgroup, each with one 16-row query tile, or with TPW > 1 an
+// even share of the group's n_tiles tiles (every K/V fragment read from LDS
+// then serves all of a wave's tiles), NS LDS stages (3 here).  bf16 products:
+// unit u is computed from stage u % NS while units u + 1 .. u + NS - 1 are in
+// flight.  F16: at step u the workgroup converts unit u + 1 to fp16 in LDS
+// while it computes unit u, units u + 2 .. u + NS - 1 in flight, so each K/V
+// element is converted once for all W waves and every product is a single
+// fp16 MFMA (half the matrix-core work of the hi + lo bf16 pairs).
+template <int HD, int W, bool ROT, bool F16, int NS, int TPW>
 __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   constexpr int NC = HD / 32, NT = HD / 16;
   constexpr int NI = UnitLayout<HD>::NI;
   constexpr int PPL = (NI + W - 1) / W;  // wave-instructions per wave per unit
+  constexpr int D = NS - 1;              // issue distance in units
   static_assert(W <= 2 * NI, "a wave must have at least one distinct instruction slot");
-  __shared__ u32x4 stage[3][UnitLayout<HD>::PIECES];
+  static_assert(NS >= 3 && (NS - 2) * PPL < 64, "stages");
+  __shared__ u32x4 stage[NS][UnitLayout<HD>::PIECES];
   __shared__ int blk_ids[2][kIdWin];  // physical blocks of the split (rolling windows)
 
   const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, la = lane >> 4;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   __builtin_assume(tid < 64 * W);
   __builtin_assume(wave >= 0 && wave < W);
-  // Grid (KV head + n_kv * query group, split, sequence): workgroups are dealt
+  // Grid (KV head + n_kv * query group, split, sequence slot): workgroups are dealt
   // to the 8 XCDs round-robin in linear order, so with n_kv a multiple of 8
   // each XCD takes whole KV heads (the same work for every head), and the
   // query groups of one (sequence, KV head, split), which read the same K/V,
@@ -267,27 +331,38 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   // fall on the same XCDs.
   const int s = blockIdx.y;
   const int g = blockIdx.x % p.n_kv, qg = blockIdx.x / p.n_kv;
-  const int b = blockIdx.z;
+  // sequence slots run longest sequence first: the longest splits start in the
+  // first round and the short ones fill the end of the launch
+  const int b = p.order ? __builtin_amdgcn_readfirstlane(p.order[blockIdx.z]) : blockIdx.z;
   if (p.err && *p.err) return;
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int t0 = s * p.split_len;
   if (s > 0 && t0 >= n) return;
   const int t1 = min(n, t0 + p.split_len);
-  const int row0 = (qg * W + wave) * 16;     // first of this wave's rows in the KV head
+  // this wave's query tiles: [tb, tb + ntw) of the group's n_tiles (one each
+  // when TPW = 1, else an even share of at most TPW)
+  const int tb = TPW == 1 ? wave : wave * p.n_tiles / W;
+  const int ntw = TPW == 1 ? 1 : (wave + 1) * p.n_tiles / W - tb;
+  const int row0 = (qg * p.n_tiles + tb) * 16;  // first of this wave's rows in the KV head
   const int bs = 1 << p.bs_log2;
 
-  RowState<HD> st;
-  {
-    const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + row0 + li) * HD;
+  RowState<HD, F16> st[TPW];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) st[t].o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st[t].m = kNegBig;
+    st[t].l = 0.f;
+    if (t >= ntw) continue;
+    const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + row0 + 16 * t + li) * HD;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      st.qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qo + 8 * (la * NC + c)));
-      st.ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qo + 8 * (la * NC + c)));
-    }
+      st[t].qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qo + 8 * (la * NC + c)));
+      st[t].ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qo + 8 * (la * NC + c)));
+      if constexpr (F16)
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) st.o[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    st.m = kNegBig;
-    st.l = 0.f;
+        for (int i = 0; i < 8; ++i) st[t].q16[c][i] = (f16)((float)st[t].qh[c][i] + (float)st[t].ql[c][i]);
+    }
   }
 
   const int nunits = (t1 - t0 + 31) >> 5;   // 0 when the split has no cache tokens
@@ -379,8 +454,17 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
       }
     };
     const int last = nunits - 1;
-    issue(0, 0);
-    if (last >= 1) issue(1, 1);
+    // wait until at most k (0 <= k <= NS - 2) units of this wave's loads remain in flight
+    auto wait_units = [&](int k) __attribute__((always_inline)) { wait_units_le<PPL, NS - 2>(k); };
+#pragma unroll
+    for (int v = 0; v < D; ++v)
+      if (v <= last) issue(v, v);
+    if constexpr (F16) {
+      // unit 0 converted before the loop (its conversion is published by step 0's barrier)
+      wait_units(min(D - 1, last));
+      lds_barrier();
+      convert_unit<HD, W>(stage[0], t1 - t0, tid);
+    }
     int buf = 0;
     // One unit: wait for its loads, publish them, issue unit u + 2, compute.
     // The first unit is peeled (raw scores; see qk_unit).
@@ -402,46 +486,65 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
       else if (pr == 1) __builtin_amdgcn_s_setprio(1);
       else __builtin_amdgcn_s_setprio(2);
     };
+    // Entering window w >= 1 of the block ids when issuing unit v: load window
+    // w + 1 (it replaces window w - 1, which no later issue reads).  Loads issued
+    // after the unit's only make the next vmcnt waits stricter.
+    auto next_window = [&](int v) __attribute__((always_inline)) {
+      const int w = (((t0 + 32 * v) >> p.bs_log2) - lb0) / kIdWin;
+      const int wprev = (((t0 + 32 * (v - 1)) >> p.bs_log2) - lb0) / kIdWin;
+      if (bt_row && w != wprev && (w + 1) * kIdWin < nlb) load_window(w + 1);
+    };
     auto step = [&](int u, auto first) __attribute__((always_inline)) {
-      // this wave's loads of unit u are done once at most those of unit u + 1 remain
-      if (u < last)
-        wait_vmcnt<PPL>();
-      else
-        wait_vmcnt<0>();
-      // every wave's loads of unit u have landed and every wave is done with unit u - 1
-      lds_barrier();
-      if constexpr (ROT)
-        if ((u & 3) == 0) rotate_priority();
       const int limit = t1 - (t0 + 32 * u);
-      if (limit < 32) {
-        zero_tail<HD, W>(stage[buf], limit, tid);
+      // units issued so far: 0 .. min(u + D - 1, last)
+      const int issued = min(u + D - 1, last);
+      if constexpr (!F16) {
+        // this wave's loads of unit u are done once at most those of the later issued units remain
+        wait_units(issued - u);
+        // every wave's loads of unit u have landed and every wave is done with unit u - 1
         lds_barrier();
+        if constexpr (ROT)
+          if ((u & 3) == 0) rotate_priority();
+        if (limit < 32) {
+          zero_tail<HD, W>(stage[buf], limit, tid);
+          lds_barrier();
+        }
+      } else {
+        // this wave's loads of unit u + 1 are done once at most those of the later issued units remain
+        wait_units(max(issued - u - 1, 0));
+        // every wave's loads of unit u + 1 have landed, unit u's conversion is
+        // visible, every wave is done with unit u - 1
+        lds_barrier();
+        if constexpr (ROT)
+          if ((u & 3) == 0) rotate_priority();
       }
-      if (u + 2 <= last) {
-        issue(u + 2, buf == 0 ? 2 : buf - 1);
-        // entering window w >= 1 of the block ids: load window w + 1 (it
-        // replaces window w - 1, which no later unit reads).  Loads issued
-        // after the unit's only make the next vmcnt waits stricter.
-        const int w = (((t0 + 32 * (u + 2)) >> p.bs_log2) - lb0) / kIdWin;
-        const int wprev = (((t0 + 32 * (u + 1)) >> p.bs_log2) - lb0) / kIdWin;
-        if (bt_row && w != wprev && (w + 1) * kIdWin < nlb) load_window(w + 1);
+      // unit u + D into the stage of unit u - 1
+      if (u + D <= last) {
+        issue(u + D, buf == 0 ? NS - 1 : buf - 1);
+        next_window(u + D);
       }
-      compute_unit<HD, decltype(first)::value>(st, stage[buf], limit, li, la);
-      buf = buf == 2 ? 0 : buf + 1;
+      if constexpr (F16)
+        if (u + 1 <= last) convert_unit<HD, W>(stage[buf == NS - 1 ? 0 : buf + 1], limit - 32, tid);
+      compute_unit<HD, decltype(first)::value, F16, TPW>(st, ntw, stage[buf], limit, li, la);
+      buf = buf == NS - 1 ? 0 : buf + 1;
     };
     step(0, std::true_type{});
     for (int u = 1; u < nunits; ++u) step(u, std::false_type{});
   }
 
-  const int64_t prow = (((int64_t)b * p.n_kv + g) * p.max_splits + s) * p.r_alloc + row0;
-  float lt = st.l;
-  lt += __shfl_xor(lt, 16);
-  lt += __shfl_xor(lt, 32);
-  if (la == 0) p.ml_part[prow + li] = make_float2(st.m, lt);
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
+  for (int t = 0; t < TPW; ++t) {
+    if (t >= ntw) continue;
+    const int64_t prow = (((int64_t)b * p.n_kv + g) * p.max_splits + s) * p.r_alloc + row0 + 16 * t;
+    float lt = st[t].l;
+    lt += __shfl_xor(lt, 16);
+    lt += __shfl_xor(lt, 32);
+    if (la == 0) p.ml_part[prow + li] = make_float2(st[t].m, lt);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) p.o_part[(prow + 4 * la + r) * HD + 16 * nt + li] = st.o[nt][r];
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) p.o_part[(prow + 4 * la + r) * HD + 16 * nt + li] = st[t].o[nt][r];
+  }
 }
 
 // ---------------------------------------------------------------- fp32 path
@@ -541,37 +644,73 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
   }
 }
 
+// One workgroup: the rank of each sequence by clamped length, longest first,
+// ties by index (a deterministic permutation).
+__global__ __launch_bounds__(1024) void order_by_length(const int* seq_lens, int batch, int max_seq_len,
+                                                        int* order) {
+  for (int b = threadIdx.x; b < batch; b += blockDim.x) {
+    const int nb = clamp_len(seq_lens, b, max_seq_len);
+    int rank = 0;
+    for (int o = 0; o < batch; ++o) {
+      const int no = clamp_len(seq_lens, o, max_seq_len);
+      rank += (no > nb) || (no == nb && o < b);
+    }
+    order[rank] = b;
+  }
+}
+
 }  // namespace
 
+hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t s) {
+  if (batch <= 0) return hipSuccess;
+  hipLaunchKernelGGL(order_by_length, dim3(1), dim3(1024), 0, s, seq_lens, batch, max_seq_len, order);
+  return hipGetLastError();
+}
+
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s) {
+  const bool f16 = p.f16;
+  const int stages = p.stages;
+  // query tiles per wave (the group's n_tiles over its waves)
+  const int tpw = (p.n_tiles + waves - 1) / waves;
+  if (p.n_tiles < waves || tpw > 4) return hipErrorInvalidValue;
   if (p.bs_log2 < 4 || p.split_len % 32) return hipErrorInvalidValue;
   const dim3 grid(p.n_kv * p.n_qgroups, p.max_splits, batch);
+  if (p.n_qgroups * p.n_tiles * 16 != p.r_alloc) return hipErrorInvalidValue;
   // Rotating priorities pays where several multi-wave workgroups share each
   // compute unit for the whole launch: a grid of at most one round (long
   // uniform batches: 83% of HBM peak against 78%).  Grids of many rounds
   // refill compute units as workgroups end, and one-wave workgroups do not
   // stagger; there the clock reads only cost time (2-5% measured).
   if (p.num_cus < 1) return hipErrorInvalidValue;
-  const int per_cu = attn_wgs_per_cu(hd, waves);
+  const int per_cu = attn_wgs_per_cu(hd, waves, tpw);
   const bool rot = waves >= 2 && per_cu >= 2 && (int64_t)grid.x * grid.y * grid.z <= (int64_t)p.num_cus * per_cu;
 #define SP_ATTN_CASE(HD_, W_)                                                                 \
-  if (hd == HD_ && waves == W_) {                                                             \
-    hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false>), grid, dim3(64 * W_), 0, s, p);       \
+  if (!f16 && hd == HD_ && waves == W_ && tpw == 1 && stages == 3) {                          \
+    hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false, false, 3, 1>), grid, dim3(64 * W_), 0, s, p); \
     return hipGetLastError();                                                                 \
   }
 #define SP_ATTN_CASE_ROT(HD_, W_)                                                             \
-  if (hd == HD_ && waves == W_) {                                                             \
-    if (rot) hipLaunchKernelGGL((attn_split_bf16<HD_, W_, true>), grid, dim3(64 * W_), 0, s, p); \
-    else hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false>), grid, dim3(64 * W_), 0, s, p);    \
+  if (!f16 && hd == HD_ && waves == W_ && tpw == 1 && stages == 3) {                          \
+    if (rot) hipLaunchKernelGGL((attn_split_bf16<HD_, W_, true, false, 3, 1>), grid, dim3(64 * W_), 0, s, p); \
+    else hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false, false, 3, 1>), grid, dim3(64 * W_), 0, s, p);    \
     return hipGetLastError();                                                                 \
   }
-  // rot can hold only where a compute unit takes two workgroups or more
+#define SP_ATTN_CASE_MULTI(HD_, W_, TPW_)                                                     \
+  if (hd == HD_ && waves == W_ && tpw == TPW_ && stages == 3) {                              \
+    if (f16) hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false, true, 3, TPW_>), grid, dim3(64 * W_), 0, s, p); \
+    else hipLaunchKernelGGL((attn_split_bf16<HD_, W_, false, false, 3, TPW_>), grid, dim3(64 * W_), 0, s, p);    \
+    return hipGetLastError();                                                                 \
+  }
+  // several query tiles per wave (8-16 tiles per group on 4 waves; fp16 products)
+  SP_ATTN_CASE_MULTI(128, 4, 2) SP_ATTN_CASE_MULTI(128, 4, 3)
+  SP_ATTN_CASE_MULTI(64, 4, 2) SP_ATTN_CASE_MULTI(64, 4, 3) SP_ATTN_CASE_MULTI(64, 4, 4)
+  // one tile per wave (up to 6 tiles per group; rot can hold only where a
+  // compute unit takes two workgroups or more)
   SP_ATTN_CASE(128, 1) SP_ATTN_CASE_ROT(128, 2) SP_ATTN_CASE_ROT(128, 3) SP_ATTN_CASE_ROT(128, 4)
-  SP_ATTN_CASE_ROT(128, 5) SP_ATTN_CASE_ROT(128, 6) SP_ATTN_CASE(128, 8) SP_ATTN_CASE(128, 10)
-  SP_ATTN_CASE(128, 12)
+  SP_ATTN_CASE_ROT(128, 5) SP_ATTN_CASE_ROT(128, 6)
   SP_ATTN_CASE(64, 1) SP_ATTN_CASE_ROT(64, 2) SP_ATTN_CASE_ROT(64, 3) SP_ATTN_CASE_ROT(64, 4)
-  SP_ATTN_CASE_ROT(64, 5) SP_ATTN_CASE_ROT(64, 6) SP_ATTN_CASE_ROT(64, 8) SP_ATTN_CASE_ROT(64, 10)
-  SP_ATTN_CASE(64, 12) SP_ATTN_CASE(64, 16)
+  SP_ATTN_CASE_ROT(64, 5) SP_ATTN_CASE_ROT(64, 6)
+#undef SP_ATTN_CASE_MULTI
 #undef SP_ATTN_CASE_ROT
 #undef SP_ATTN_CASE
   return hipErrorInvalidValue;

@@ -67,18 +67,26 @@ struct AttnParams {
   int64_t k_sb, k_sh, v_sb, v_sh;     // elements
   const int* block_table;  // nullable (contiguous)
   const int* seq_lens;
+  const int* order;        // nullable: sequence of each grid slot (longest first), from launch_order_by_length
   const int* err;          // nullable
   float* o_part;           // [B][n_kv][max_splits][r_alloc][hd] fp32, unnormalised
   float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
   int n_kv, rows, r_alloc, n_qgroups;
+  int n_tiles;             // 16-row query tiles per query group (r_alloc = n_qgroups n_tiles 16)
   int bs_log2, mbps, max_seq_len, split_len, max_splits;
   int num_cus;             // compute units of the device
+  int f16;                 // bf16 path: single fp16 products (K, V converted in LDS; Q, P in fp16)
+  int stages;              // bf16 path: LDS stages of the load pipeline (3)
 };
-// Workgroups of the bf16 attention kernel one compute unit holds: three by LDS,
-// and at most 12 waves (head_dim 128) or 20 (64) by VGPRs.
-inline int attn_wgs_per_cu(int hd, int waves) {
-  const int by_vgprs = (hd == 128 ? 12 : 20) / waves;
-  return by_vgprs < 3 ? by_vgprs : 3;
+// Workgroups of the bf16 attention kernel one compute unit holds: by LDS (160 KB;
+// three stages, each a 32-token unit of K and V: 16.4 KB at head_dim 128) and by
+// VGPRs: one query tile per wave takes ~150 (12 waves per compute unit at
+// head_dim 128, 20 at 64), several tiles per wave ~250 (8 waves).
+inline int attn_wgs_per_cu(int hd, int waves, int tiles_per_wave = 1) {
+  const int stage_bytes = (hd == 128 ? 1028 : 516) * 16;
+  const int by_lds = (160 * 1024) / (3 * stage_bytes + 4096);
+  const int by_vgprs = (tiles_per_wave > 1 ? 8 : (hd == 128 ? 12 : 20)) / waves;
+  return by_vgprs < by_lds ? by_vgprs : by_lds;
 }
 // Cache tokens only (the soft keys are folded in by the merge).
 // bf16-storage path (bf16 MFMA, split Q and P): head_dim 64/128, `waves` 16-row
@@ -86,6 +94,9 @@ inline int attn_wgs_per_cu(int hd, int waves) {
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s);
 // fp32 VALU path: head_dim 64/128, rows <= 64.
 hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);
+// order[r] = the sequence of rank r when the batch is sorted by clamped length,
+// longest first, ties by index (a permutation of 0..batch-1).
+hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t s);
 
 struct MergeParams {
   const float* o_part;

@@ -88,7 +88,10 @@ void image_header(const sp_probe_config& c, uint32_t (&w)[kHeaderWords]) {
 
 // Attention launch shape for `rows` query rows per KV head.
 struct AttnPlan {
-  int rows, waves, n_qgroups, r_alloc, split_len, max_splits;
+  int rows, n_qgroups, r_alloc, split_len, max_splits;
+  int tiles;  // 16-row query tiles per query group
+  int waves;  // waves per workgroup (bf16 storage; tiles / waves query tiles per wave)
+  int f16;    // bf16 storage: single fp16 products (matrix-core-bound shapes)
 };
 
 struct Plan {
@@ -102,6 +105,7 @@ struct Plan {
   // rows and their inputs
   size_t off_rq, off_rq_lo, off_rks, off_rks_lo, off_rvs, off_rvs_lo, off_rqkv, off_ru, off_rhn,
       off_ren, off_rce, off_rx, off_r3, off_rh0, off_rscale;
+  size_t off_order;               // sequences ordered longest first (int32 [max_batch])
   size_t off_gpart, gpart_bytes;  // split-K partial sums of the small-row projections
   size_t off_guard_tab;           // device table of the guard offsets
   size_t guard_off[kMaxGuards];
@@ -152,11 +156,11 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows, int num_cus) {
     a.n_qgroups = 1;
     a.r_alloc = rows;
   } else {
-    // one wave per 16-row query tile, at most 12 (head_dim 128: a compute unit
-    // holds 12 waves of its ~150 VGPRs) or 16 (64) waves per workgroup, so one
-    // workgroup reads each K/V tile for as many rows as fit (the 160 rows of
-    // the 27B shape as one group of ten: 28% faster than two groups of five);
-    // the sizes below are the instantiated ones (extra tiles are padding)
+    // 16-row query tiles per group: at most 12 (head_dim 128) or 16 (64), so
+    // one workgroup reads each K/V tile for as many rows as fit (the 160 rows
+    // of the 27B shape as one group of ten tiles: a second group would read
+    // the cache twice); the sizes below are the planned ones (extra tiles are
+    // padding).  Up to 6 tiles: one wave per tile.
     static const int kWaves[] = {1, 2, 3, 4, 5, 6, 8, 10, 12, 16};
     const int max_w = c.head_dim == 128 ? 12 : 16;
     const int groups = (tiles + max_w - 1) / max_w;
@@ -164,9 +168,20 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows, int num_cus) {
     int w = max_w;
     for (int cand : kWaves)
       if (cand >= per_group) { w = cand; break; }
+    a.tiles = w;
     a.waves = w;
     a.n_qgroups = (tiles + w - 1) / w;
     a.r_alloc = a.n_qgroups * w * 16;
+    // Eight or more tiles per group (the 160 rows of the 27B shape, several
+    // tasks): one wave per SIMD, each carrying 2-4 tiles, so every K/V fragment
+    // read from LDS serves several tiles, with the K/V tiles converted to fp16
+    // once in LDS and single fp16 products (27B shape: 3.2 ms against 5.0 ms for
+    // ten waves of one tile; hi + lo bf16 products at 2-4 tiles per wave are
+    // matrix-core bound and gain nothing).
+    if (w >= 8) {
+      a.waves = 4;
+      a.f16 = 1;
+    }
   }
   if (c.split_len) {
     a.split_len = c.split_len;
@@ -176,7 +191,7 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows, int num_cus) {
     // sequence: three splits for the longest sequences measured faster than
     // one, two or four on uniform and ragged batches alike, whether the grid
     // is one round or many.  At least 1024 tokens, a multiple of 256.
-    const int64_t per_cu = attn_wgs_per_cu(c.head_dim, a.waves);
+    const int64_t per_cu = attn_wgs_per_cu(c.head_dim, a.waves, (a.tiles + a.waves - 1) / a.waves);
     const int64_t slots = (int64_t)num_cus * std::max<int64_t>(per_cu, 1);
     const int64_t items = (int64_t)c.max_batch * c.n_kv_heads * a.n_qgroups;
     const int64_t want = ((int64_t)c.max_seq_len * items + slots - 1) / slots;
@@ -269,6 +284,7 @@ Plan make_plan(const sp_probe_config& c, int num_cus) {
   p.off_r3 = take(B * 3 * d * e);
   p.off_rh0 = take(B * d * 4);
   p.off_rscale = take(B * 4);
+  p.off_order = take(B * 4);
   const size_t widest = std::max({(size_t)2 * c.intermediate, (size_t)p.nqkv, d});
   p.gpart_bytes = 16 * 32 * widest * 4;
   p.off_gpart = take(p.gpart_bytes);
@@ -449,10 +465,14 @@ AttnParams attn_params(const Ctx& x, const AttnPlan& a, const sp_kv_cache* kv,
   ap.o_part = o_part;
   ap.ml_part = ml_part;
   ap.n_kv = c.n_kv_heads; ap.rows = a.rows;
-  ap.r_alloc = a.r_alloc; ap.n_qgroups = a.n_qgroups;
+  ap.r_alloc = a.r_alloc; ap.n_qgroups = a.n_qgroups; ap.n_tiles = a.tiles;
   ap.bs_log2 = ilog2(kv->block_size); ap.mbps = kv->max_blocks_per_seq;
   ap.max_seq_len = c.max_seq_len; ap.split_len = a.split_len; ap.max_splits = a.max_splits;
   ap.num_cus = x.n_cus;
+  ap.f16 = a.f16;
+  ap.stages = 3;
+  // bf16 path: sequence slots in the order launch_order_by_length wrote
+  ap.order = c.dtype == SP_BF16 ? at<int>(x, x.plan->off_order) : nullptr;
   return ap;
 }
 
@@ -734,14 +754,16 @@ int forward_one_pass(const Ctx& x, const sp_kv_cache* kv, const int32_t* seq_len
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 1: split attention over the cached K/V
+  // stage 1: split attention over the cached K/V, longest sequences first
   const AttnParams ap = attn_params(x, ak, kv, seq_lens, block_table, errp, at<void>(x, pl.off_q),
                                     at<void>(x, pl.off_q_lo), at<float>(x, pl.off_opart),
                                     at<float2>(x, pl.off_ml));
-  if (dt == kBF16)
+  if (dt == kBF16) {
+    SP_TRY(launch_order_by_length(seq_lens, B, c.max_seq_len, at<int>(x, pl.off_order), s));
     SP_TRY(launch_attention_bf16(ap, hd, ak.waves, B, s));
-  else
+  } else {
     SP_TRY(launch_attention_f32(ap, hd, B, s));
+  }
   if (!mark()) return SP_ERR_HIP;
 
   // stage 2: merge the splits and each task's soft keys into the attention output rows
@@ -906,6 +928,9 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
     SP_TRY(launch_rmsnorm_rows(kF32, dt, at_dt, h0, d, fusion->fc_norm_hidden, nullptr, hn, d, B, d,
                                c.rms_eps, status, s));
   }
+
+  // the attention of every step runs its sequence slots longest first
+  if (dt == kBF16) SP_TRY(launch_order_by_length(seq_lens, B, c.max_seq_len, at<int>(x, pl.off_order), s));
 
   for (int t = 0; t < K; ++t) {
     // stage 0: x_t = W_fc[:, :d] RMSNorm(h; gamma_h) + c_t, its RMSNorm, Q/K/V, RoPE at N_b + t

@@ -120,12 +120,20 @@ static void attn_common(const AttnParams& p, int hd, int batch, size_t e) {
   if (e == 2) g.range(p.q_lo, rows * hd * e, "attention q_lo");
   g.range(p.o_part, rows * p.max_splits * hd * 4, "attention o_part");
   g.range(p.ml_part, rows * p.max_splits * 8, "attention ml_part");
+  g.range(p.order, (size_t)batch * 4, "attention order");
 }
 
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t) {
-  g.expect(p.n_qgroups * waves * 16 == p.r_alloc, "attention tiles");
+  g.expect(p.n_qgroups * p.n_tiles * 16 == p.r_alloc && p.n_tiles >= waves && p.n_tiles <= 4 * waves,
+           "attention tiles");
   g.expect(p.split_len % 32 == 0, "split_len multiple of the unit");
   attn_common(p, hd, batch, 2);
+  return hipSuccess;
+}
+
+hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t) {
+  (void)seq_lens; (void)max_seq_len;
+  g.range(order, (size_t)batch * 4, "sequence order");
   return hipSuccess;
 }
 
