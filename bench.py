@@ -45,7 +45,7 @@ DTYPE_LABEL = {"bf16": "bf16 storage; fp16xfp16->fp32 MFMA projections (fp16 ima
                        "fp32 softmax, norms, residual stream and logits",
                "f32": "f32"}
 ROTATE_BELOW = 1 << 30      # KV caches smaller than this are rotated over copies
-ATTN_SRC = os.path.join(ROOT, "paper_2608_28099_amd", "csrc", "attention.hip")
+ATTN_SRCS = [os.path.join(ROOT, "paper_2608_28099_amd", "csrc", f) for f in ("attention.hip", "merge.hip")]
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -70,19 +70,23 @@ def parse():
 
 
 def attention_source_hash() -> str:
-    return hashlib.sha256(open(ATTN_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in ATTN_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def traffic_per_launch(workload: str):
-    """HBM bytes per attention launch from committed counter runs on this
-    workload, if they were taken on the current attention source; else None."""
+    """HBM bytes per attention stage (split kernel + merge) from committed
+    counter runs on this workload, if they were taken on the current attention
+    and merge sources; else None."""
     try:
         rec = json.load(open(os.path.join(PROFILES, f"attention_{workload}_traffic.json")))
     except (OSError, ValueError):
         return None
     if rec.get("attention_src_sha256_16") != attention_source_hash():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("hbm_bytes_per_stage")
 
 
 def projection_rates(w, T, args, recursive, stages, n_fwd):

@@ -203,3 +203,30 @@ def test_packed_image_size():
     assert lib.sp_probe_pack_weights(ctypes.byref(binding.make_config(configs.TINY_F32)), ctypes.byref(wt),
                                      None, 0, None) == -2
     assert lib.sp_probe_pack_weights(ctypes.byref(cfg), ctypes.byref(wt), None, 0, None) == -1
+
+
+def test_sp1_trainable_tensors_are_table_1s_count():
+    """Table 1 (PII detection, 9B base, d = 4096): SP-1 with a one-logit linear head
+    trains 8.2K numbers, 50x fewer than MultiMax's 412K.  The trainable inputs the
+    C ABI takes are the soft prompt [k][d], w_cls [C][d] and the optional b_cls [C];
+    drawn for k = 1, C = 1 at d = 4096 they hold 8,192 numbers (8,193 with the
+    bias); every other tensor of the call is the frozen head.  Sec. 1's k = 5 soft
+    vectors at the stated d = 3584 are 17,920, the quoted figure of about 18K."""
+    from paper_2608_28099_amd import inputs
+
+    hdr = open(os.path.join(ROOT, "include", "sp_probe.h")).read()
+    assert "soft_prompt device [k][d]" in hdr and "w_cls[C][d], b_cls[C]" in hdr
+    names = ("soft_prompt", "w_cls", "b_cls")
+    w = configs.QWEN9B_BF16.replace(name="sp1_c1", k=1, n_classes=1, cls_bias=False)
+    assert w.hidden == 4096
+    p = inputs.params(w, "cpu", only=names)
+    shapes = {n: tuple(t.shape) for n, t in p.items() if t is not None}
+    assert shapes == {"soft_prompt": (1, 4096), "w_cls": (1, 4096)}
+    n = sum(t.numel() for t in p.values() if t is not None)
+    assert n == 8192 and f"{n / 1000:.1f}K" == "8.2K"
+    pb = inputs.params(w.replace(cls_bias=True), "cpu", only=names)
+    nb = sum(t.numel() for t in pb.values() if t is not None)
+    assert nb == 8193 and f"{nb / 1000:.1f}K" == "8.2K"
+    assert round(412_000 / n) == 50
+    p5 = inputs.params(w.replace(k=5, hidden=3584), "cpu", only=("soft_prompt",))
+    assert p5["soft_prompt"].numel() == 17920 and round(p5["soft_prompt"].numel(), -3) == 18000

@@ -315,14 +315,6 @@ def test_batch_order_invariance():
     np.testing.assert_array_equal(O.probe_batch([kv[i] for i in perm], x, W, shape), ref[perm])
 
 
-def test_trainable_parameter_counts():
-    """SP-1 on the 9B head (d = 4096) trains one soft vector and one head vector:
-    8192 parameters, the "8.2K" of Table 1; k = 5 soft vectors at d = 3584 are 17920,
-    the "about 18K" of Sec. 1."""
-    assert 1 * 4096 + 4096 == 8192
-    assert 5 * 3584 == 17920
-
-
 def test_tasks_are_independent_probes():
     """Sec. 3.3: classifiers sharing one cache are independent: task t's logits are
     the single-task probe's with its own soft prompt and head, whatever the other
