@@ -1,6 +1,6 @@
 // Merge of the split-attention partials with the soft keys themselves
 // (Sec. 3.3, Eq. 1-3).  Per query row the merge computes the soft keys visible
-// to it (causal: key j' <= j) in fp32 and combines them with the splits' partials
+// to it (causal: key j' <= j) and combines them with the splits' partials
 // (running max m_s in log2 units, sum l_s, unnormalised O_s) by the
 // log-sum-exp rule
 //   M = max(m_soft, max_s m_s),  L = l_soft 2^(m_soft-M) + sum_s l_s 2^(m_s-M),
@@ -32,7 +32,7 @@ __device__ __forceinline__ void soft_load_vec(const void* hi, const void* lo, in
   }
 }
 
-// One workgroup per (sequence b, KV head g, block of rw consecutive soft rows
+// VALU merge (the fp32 path).  One workgroup per (sequence b, KV head g, block of rw consecutive soft rows
 // with queries of one task): its rows see soft keys [j_lo, j] of their task (at
 // most 64), and the workgroup stages the union, [j_lo, j of its last row], once
 // in LDS as fp32 (keys and values; from the stored operands: fp32, or bf16
@@ -196,6 +196,172 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
     if (__any(oor) && lane == 0 && p.status) atomicOr(p.status, kStatusRange);
 }
 
+// bf16 path: the same merge with the soft-key attention on the matrix cores.
+// One wave per 16-row query tile of a (sequence b, KV head g, task); the rows of
+// a task are rows [task R, task R + R) of the (b, g) block, R = q_per_task group.
+// Scores come transposed, S^T = K Q^T (keys along M, query rows along N), from
+// bf16 hi + lo operands in three products (hi hi + hi lo + lo hi; the dropped
+// lo lo term is below 2^-16 of the product), so lane l holds the scores of row
+// l%16 with keys 16 kt + 4(l/16) + r.  P^T then feeds O^T = V^T P^T directly as
+// the B operand: an MFMA's K index may be any fixed permutation of the keys as
+// long as A uses the same one, so lane l's eight keys of a 32-key chunk are
+// 4(l/16) + r and 16 + 4(l/16) + r, and the A operand reads V^T at exactly
+// those keys.  V^T (hi, lo) is staged transposed in LDS once per workgroup,
+// keys past the window as zeros; K and Q fragments are 16-byte loads straight
+// from the soft operands.  O^T lands with lane l holding dims 16 dt + 4(l/16) + r
+// of row l%16, which is also how it reads that row's split partials (16 bytes
+// per dim tile) and writes its fp16 output (8 bytes).
+template <int HD>
+__global__ __launch_bounds__(256) void merge_soft_mfma(const MergeParams p) {
+  constexpr int NC = HD / 32, NDT = HD / 16;
+  extern __shared__ uint16_t vt[];  // [2][HD][ldk] bf16 bits: V^T hi, then lo
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, li = lane & 15, la = lane >> 4;
+  const int g = blockIdx.y, b = blockIdx.z;
+  if (p.err && *p.err) return;
+  const int R = p.q_per_task * p.group;
+  const int tiles = (R + 15) >> 4, wpt = (tiles + 3) >> 2;  // query tiles, workgroups per task
+  const int task = blockIdx.x / wpt, t = (blockIdx.x % wpt) * 4 + wave;
+  const int j_lo = task * p.k_task;
+  const int nk_all = p.q_first + p.q_per_task + p.step;  // keys [j_lo, j_lo + nk_all)
+  const int nkp = (nk_all + 31) & ~31, ldk = nkp + 4;
+
+  // stage V^T: consecutive lanes take consecutive keys of one 8-dim chunk
+  const int64_t vo = (((p.per_seq ? (int64_t)b * p.n_kv : 0) + g) * p.ks + j_lo) * HD;
+  for (int e = threadIdx.x; e < nkp * (HD / 8); e += blockDim.x) {
+    const int key = e % nkp, d0 = (e / nkp) * 8;
+    u32x4 h = {0, 0, 0, 0}, l = {0, 0, 0, 0};
+    if (key < nk_all) {
+      h = ld16v((const bf16*)p.v_soft + vo + (int64_t)key * HD + d0);
+      l = ld16v((const bf16*)p.v_soft_lo + vo + (int64_t)key * HD + d0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      vt[(d0 + i) * ldk + key] = (uint16_t)(h[i >> 1] >> (16 * (i & 1)));
+      vt[(HD + d0 + i) * ldk + key] = (uint16_t)(l[i >> 1] >> (16 * (i & 1)));
+    }
+  }
+  __syncthreads();
+  if (t >= tiles) return;
+
+  const int r = 16 * t + li;               // this lane's query row within the task (column of S^T)
+  const bool valid = r < R;
+  const int rr = valid ? r : R - 1;        // padding columns repeat the last row; never stored
+  const int64_t bg = (int64_t)b * p.n_kv + g;
+  const int64_t qrow = bg * p.r_alloc + (int64_t)task * R + rr;
+  bf16x8 qh[NC], ql[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qrow * HD + 32 * c + 8 * la));
+    ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qrow * HD + 32 * c + 8 * la));
+  }
+  const int64_t ko = (bg * p.ks + j_lo) * HD;
+  const int nkt = (nk_all + 15) >> 4;
+  f32x4 sc[4];
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt) {
+    sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (kt < nkt) {
+      const int key = min(16 * kt + li, nk_all - 1);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const bf16x8 kh = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.k_soft + ko + (int64_t)key * HD + 32 * c + 8 * la));
+        const bf16x8 kl = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.k_soft_lo + ko + (int64_t)key * HD + 32 * c + 8 * la));
+        sc[kt] = mfma16x16x32_bf16(kh, qh[c], sc[kt]);
+        sc[kt] = mfma16x16x32_bf16(kh, ql[c], sc[kt]);
+        sc[kt] = mfma16x16x32_bf16(kl, qh[c], sc[kt]);
+      }
+    }
+  }
+  // causal window of the row: keys [j_lo, j_lo + nk_r); key j_lo always visible
+  const int nk_r = p.q_first + (rr / p.group) % p.q_per_task + p.step + 1;
+  float M = kNegBig;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (16 * kt + 4 * la + i < nk_r) M = fmaxf(M, sc[kt][i]);
+  M = fmaxf(M, __shfl_xor(M, 16));
+  M = fmaxf(M, __shfl_xor(M, 32));
+  float L = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float pv = 16 * kt + 4 * la + i < nk_r ? fast_exp2(sc[kt][i] - M) : 0.f;
+      sc[kt][i] = pv;
+      L += pv;
+    }
+  L += __shfl_xor(L, 16);
+  L += __shfl_xor(L, 32);
+
+  f32x4 o[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    if (32 * c2 < nk_all) {
+      bf16x8 ph, pl;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float pv = sc[2 * c2 + (i >> 2)][i & 3];
+        ph[i] = (bf16)pv;
+        pl[i] = (bf16)(pv - (float)ph[i]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const uint16_t* vr = vt + (16 * dt + li) * ldk + 32 * c2 + 4 * la;
+        const u32x2 h0 = *reinterpret_cast<const u32x2*>(vr), h1 = *reinterpret_cast<const u32x2*>(vr + 16);
+        const u32x2 l0 = *reinterpret_cast<const u32x2*>(vr + HD * ldk);
+        const u32x2 l1 = *reinterpret_cast<const u32x2*>(vr + HD * ldk + 16);
+        const bf16x8 vh = __builtin_bit_cast(bf16x8, u32x4{h0.x, h0.y, h1.x, h1.y});
+        const bf16x8 vl = __builtin_bit_cast(bf16x8, u32x4{l0.x, l0.y, l1.x, l1.y});
+        o[dt] = mfma16x16x32_bf16(vh, ph, o[dt]);
+        o[dt] = mfma16x16x32_bf16(vh, pl, o[dt]);
+        o[dt] = mfma16x16x32_bf16(vl, ph, o[dt]);
+      }
+    }
+  }
+  if (!valid) return;
+
+  // the splits' partials, by the log-sum-exp rule
+  const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
+  const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
+  const int64_t base = bg * p.max_splits * p.r_alloc + (int64_t)task * R + r;
+  float Mt = M;
+  for (int sp = 0; sp < ns; ++sp) Mt = fmaxf(Mt, p.ml_part[base + (int64_t)sp * p.r_alloc].x);
+  const float a0 = fast_exp2(M - Mt);
+  L *= a0;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) o[dt] *= a0;
+  for (int sp = 0; sp < ns; ++sp) {
+    const int64_t row = base + (int64_t)sp * p.r_alloc;
+    const float2 ml = p.ml_part[row];
+    const float w = fast_exp2(ml.x - Mt);
+    L += ml.y * w;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const float4 v = *reinterpret_cast<const float4*>(p.o_part + row * HD + 16 * dt + 4 * la);
+      o[dt] += f32x4{v.x, v.y, v.z, v.w} * w;
+    }
+  }
+  const float inv = 1.0f / L;
+  const int qi = task * p.q_per_task + r / p.group, h = g * p.group + r % p.group;
+  f16* out = (f16*)p.out + ((int64_t)b * p.out_rows + p.out_off + qi) * ((int64_t)p.n_q * HD) + (int64_t)h * HD + 4 * la;
+  bool oor = false;
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) {
+    f16x4 y;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float v = o[dt][i] * inv;
+      oor |= !(fabsf(v) <= 65504.0f);
+      y[i] = (f16)v;
+    }
+    *reinterpret_cast<f16x4*>(out + 16 * dt) = y;
+  }
+  if (__any(oor) && lane == 0 && p.status) atomicOr(p.status, kStatusRange);
+}
+
 }  // namespace
 
 hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s) {
@@ -205,12 +371,22 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
   if (nk_max > 64 || p.rows % p.group) return hipErrorInvalidValue;
   if (p.q_per_task < 1 || (p.rows / p.group) % p.q_per_task) return hipErrorInvalidValue;
   const int tasks = p.rows / p.group / p.q_per_task;
-  // Soft rows per workgroup: the most (a power of two) that still leave
-  // min_wgs workgroups (4 per compute unit).  Each workgroup stages its key
-  // window once and then streams its rows' partials; measured against 1-16
-  // workgroups per compute unit this was fastest on every workload (long
-  // context: 32 us against 44 us at one soft row per workgroup; 27B shape:
-  // 0.37 ms against 0.86 ms).
+  // bf16 storage: matrix-core merge, up to four query tiles per workgroup (one
+  // per wave), fp16 output for the o-projection's fp16 MFMA.  Against the
+  // VALU merge below on the same rows: 27B shape 0.15 ms against 0.39 ms, the
+  // ragged 9B shape 31 us against 65 us.
+  if (dt == kBF16) {
+    const int R = p.q_per_task * p.group, tiles = (R + 15) / 16;
+    const int nkp = (nk_max + 31) & ~31;
+    const dim3 grid(tasks * ((tiles + 3) / 4), p.n_kv, batch), block(64 * (tiles < 4 ? tiles : 4));
+    const size_t lds = (size_t)2 * p.hd * (nkp + 4) * sizeof(uint16_t);
+    if (p.hd == 128) hipLaunchKernelGGL(merge_soft_mfma<128>, grid, block, lds, s, p);
+    else hipLaunchKernelGGL(merge_soft_mfma<64>, grid, block, lds, s, p);
+    return hipGetLastError();
+  }
+  // fp32 path.  Soft rows per workgroup: the most (a power of two) that still
+  // leave min_wgs workgroups (4 per compute unit).  Each workgroup stages its
+  // key window once and then streams its rows' partials.
   MergeParams q = p;
   const int64_t min_wgs = p.min_wgs > 0 ? p.min_wgs : 1024;
   q.rw = 1;
@@ -222,13 +398,8 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
   const int rows_wg = q.rw * p.group;
   const dim3 block(64 * (rows_wg < 4 ? rows_wg : 4));
   const size_t lds = (size_t)2 * nk_max * p.hd * sizeof(float);  // its keys and values, fp32
-  if (dt == kBF16) {  // the attention output feeds an fp16 MFMA
-    if (p.hd == 128) hipLaunchKernelGGL((merge_splits<f16, bf16, 2>), grid, block, lds, s, q);
-    else hipLaunchKernelGGL((merge_splits<f16, bf16, 1>), grid, block, lds, s, q);
-  } else {
-    if (p.hd == 128) hipLaunchKernelGGL((merge_splits<float, float, 2>), grid, block, lds, s, q);
-    else hipLaunchKernelGGL((merge_splits<float, float, 1>), grid, block, lds, s, q);
-  }
+  if (p.hd == 128) hipLaunchKernelGGL((merge_splits<float, float, 2>), grid, block, lds, s, q);
+  else hipLaunchKernelGGL((merge_splits<float, float, 1>), grid, block, lds, s, q);
   return hipGetLastError();
 }
 
