@@ -6,7 +6,8 @@
 // (each a (BM/WGM) x (BN/WGN) sub-tile) and consumes K in steps of BK (32 or
 // 64: one or two MFMAs deep).  Each step's A and W tiles are loaded straight
 // into LDS, S - 1 steps ahead of use, through an S-stage ring (one barrier per
-// step); weights stay bf16 in LDS and are converted exactly to fp16 (|w| in
+// step; S = 2 is plain double buffering: the loads of step k + 1 are issued
+// right after the barrier of step k and waited for before the next); weights stay bf16 in LDS and are converted exactly to fp16 (|w| in
 // [2^-14, 65504]) as a wave reads its fragments.  A row of a stage tile is BK
 // values = PPR 16-byte pieces; piece kp of row r sits at
 //   r * PPR + (kp ^ ((r >> 1) & (PPR - 1)))
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lds(const GemmParams p) {
   constexpr int STAGE = (BM + BN) * PPR;             // pieces per stage
   static_assert(BK == 32 || BK == 64, "step depth");
   static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile");
-  static_assert(S >= 3 && (S - 2) * IPW < 64, "stages");
+  static_assert(S >= 2 && (S - 2) * IPW < 64, "stages");
   static_assert(EPI != kEpiSwiglu || WN % 32 == 0, "SwiGLU pairs 16 gate and 16 up columns");
   __shared__ u32x4 lds[S * STAGE];
 
@@ -295,20 +296,22 @@ hipError_t launch_tile(Epilogue epi, const GemmParams& p, int ksplit, hipStream_
   return launch_gemm_reduce(epi, p, ksplit, BN, s);
 }
 
-// Tile shapes, in order of preference (measured on the probe's projection
-// shapes, 512 to 8192 rows): (BM, BN, waves along M, waves along N, K-step
-// depth); the stage counts are in launch_tile_index.  SwiGLU (gate/up) prefers
-// the widest tiles; the residual epilogues (o, down) prefer 256 x 128 tiles with
-// 64-deep steps, which at 2048-8192 rows take half the time of 128 x 64.  The
-// 256 x 256 tile runs 2 x 4 waves: each weight fragment is then read (and, from
-// bf16 weights, converted) by two waves instead of four.  Index 9 is the
-// 32 x 128 tile of the 17-32-row products.
+// Tile shapes (BM, BN, waves along M, waves along N, K-step depth); the stage
+// counts are in launch_tile_index.  The residual epilogues (o, down) prefer
+// 256 x 128 tiles with 64-deep steps, which at 2048-8192 rows take half the
+// time of 128 x 64.  Index 9 is the 32 x 128 tile of the 17-32-row products.
+// Index 10 is 256 x 256 with 64-deep steps, double-buffered (two 64 KB stages):
+// 64-deep steps halve the barriers per unit of K and load whole 128-byte rows
+// per step (32-deep steps load half rows, and with them half cache lines), and
+// more stages measured no faster (SwiGLU, fp16 weights, 8192 x 34816 x 5120:
+// 2.35 ms against 2.59 ms for 256 x 256 in 32-deep steps; 2048 x 24576 x 4096:
+// 0.335 ms against 0.368 ms).
 struct TileShape { int bm, bn, wgm, wgn, bk; };
-constexpr int kNumTiles = 10;
+constexpr int kNumTiles = 11;
 constexpr TileShape kTiles[kNumTiles] = {
     {256, 256, 2, 4, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
     {64, 64, 2, 2, 64},   {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64},  {16, 16, 1, 1, 64},
-    {16, 32, 1, 1, 32},   {32, 128, 1, 4, 64}};
+    {16, 32, 1, 1, 32},   {32, 128, 1, 4, 64},  {256, 256, 4, 2, 64}};
 constexpr int kOrderSwiglu[9] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
 constexpr int kOrderResid[9] = {2, 1, 0, 3, 4, 5, 6, 7, 8};
 
@@ -330,6 +333,7 @@ hipError_t launch_tile_index(int c, Epilogue epi, const GemmParams& p, int kspli
     case 7: return launch_tile<16, 16, 1, 1, 8, 64>(epi, p, ksplit, s);
     case 8: return launch_tile<16, 32, 1, 1, 8, 32>(epi, p, ksplit, s);
     case 9: return launch_tile<32, 128, 1, 4, 6, 64>(epi, p, ksplit, s);
+    case 10: return launch_tile<256, 256, 4, 2, 2, 64>(epi, p, ksplit, s);
   }
   return hipErrorInvalidValue;
 }
@@ -393,11 +397,17 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     while (ks < 16 && tiles * ks * 2 <= 4 * cus && KT / (ks * 2) >= 8 && fits(ks * 2)) ks *= 2;
     return launch_tile_index(9, epi, p, ks, s);
   }
-  // Long K with a few hundred rows (the down projection of 512 rows): 256 x 128
-  // tiles with K split four ways re-read the activations and weights half as
-  // often as the 128 x 64 tiles, at the same workgroup count.
-  if (p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[2]) && fits(4))
-    return launch_tile_index(2, epi, p, 4, s);
+  // Long K with a few hundred rows (the down projection of 129-1024 rows):
+  // 256 x 128 tiles with K split re-read the activations and weights half as
+  // often as the 128 x 64 tiles, at the same workgroup count.  Four slices
+  // when two would leave at most half the compute units a workgroup, else two
+  // (512 x 4096 x 12288, 64 tiles: 82 us against 114 us for two slices;
+  // 1024 x 2560 x 9728, 80 tiles: 88 us against 100 us for four).
+  if (epi != kEpiSwiglu && p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[2])) {
+    const long tiles = (long)((p.M + 255) / 256) * (p.N / 128);
+    const int ks = tiles * 2 <= cus / 2 ? 4 : 2;
+    if (p.K % (64 * ks) == 0 && fits(ks)) return launch_tile_index(2, epi, p, ks, s);
+  }
   // 33..256 rows, epilogues other than SwiGLU (o, down, the fusion products):
   // the weights stream with few tiles, so 128 x 64 tiles with K split until
   // the grid has a workgroup per compute unit (9B-shaped down on 128 rows:
@@ -408,6 +418,26 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     int ks = 2;
     while (ks < 8 && tiles * ks < cus) ks *= 2;
     if (p.K / 64 / ks >= 8 && fits(ks)) return launch_tile_index(3, epi, p, ks, s);
+  }
+  // SwiGLU (gate/up) on more than 256 rows: the wide tiles, priced by the rounds of workgroups the
+  // grid takes on the compute units (a last partial round costs a whole one)
+  // times the tile's work over its measured relative rate (2048-8192 rows,
+  // fp16 weights).  At 1024 x 19456 x 2560 this takes 256 x 128 (608 tiles,
+  // 0.140 ms) over 256 x 256 (304 tiles: two rounds, the second nearly empty,
+  // 0.154 ms).
+  if (epi == kEpiSwiglu && p.M > 256) {
+    static const int cand[4] = {10, 0, 2, 1};
+    static const double rate[4] = {1.0, 0.91, 0.87, 0.82};
+    int best = -1;
+    double best_cost = 0.0;
+    for (int i = 0; i < 4; ++i) {
+      const TileShape& t = kTiles[cand[i]];
+      if (!tile_ok(p, epi, t)) continue;
+      const long tiles = (long)((p.M + t.bm - 1) / t.bm) * (p.N / t.bn);
+      const double cost = (double)((tiles + cus - 1) / cus) * t.bm * t.bn / rate[i];
+      if (best < 0 || cost < best_cost) { best = cand[i]; best_cost = cost; }
+    }
+    if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
   }
   // First tile (in preference order) that gives at least one workgroup per
   // compute unit, else the valid tile with the most workgroups.

@@ -285,8 +285,10 @@ Plan make_plan(const sp_probe_config& c, int num_cus) {
   p.off_rh0 = take(B * d * 4);
   p.off_rscale = take(B * 4);
   p.off_order = take(B * 4);
+  // split-K partials: up to 512 rows of the widest product, and four slices of
+  // a hidden-wide product on up to 1024 rows (o and down there split K)
   const size_t widest = std::max({(size_t)2 * c.intermediate, (size_t)p.nqkv, d});
-  p.gpart_bytes = 16 * 32 * widest * 4;
+  p.gpart_bytes = std::max(16 * 32 * widest, 4 * std::min<size_t>(M, 1024) * d) * 4;
   p.off_gpart = take(p.gpart_bytes);
   p.off_guard_tab = take(kMaxGuards * sizeof(uint64_t));
   p.total = o;
