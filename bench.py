@@ -89,9 +89,10 @@ def traffic_per_launch(workload: str):
     return rec.get("hbm_bytes_per_stage")
 
 
-def projection_rates(w, T, args, recursive, stages, n_fwd):
+def projection_rates(w, T, args, recursive, stages, n_fwd, mfma_peak):
     """Achieved MFMA throughput of the projection stages (their algorithmic FLOP
-    over the stage's mean HIP-event time per forward) against the dense peak."""
+    over the stage's mean HIP-event time per forward) against the dense peak
+    and against the rate this device's matrix cores sustain (mfma_peak)."""
     d, I, qkv = w.hidden, w.intermediate, (w.n_q_heads + 2 * w.n_kv_heads) * w.head_dim
     qw = w.n_q_heads * w.head_dim
     if recursive:   # k steps of B rows each (the fusion's B x d x d product is in soft prep)
@@ -104,7 +105,9 @@ def projection_rates(w, T, args, recursive, stages, n_fwd):
         ms = stages[name] / n_fwd
         tf = f / (ms * 1e-3) / 1e12
         out[name] = {"gflop": round(f / 1e9, 2), "ms": round(ms, 4), "tflops": round(tf, 1),
-                     "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4)}
+                     "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4),
+                     "frac_of_measured_mfma_peak": round(tf / mfma_peak, 4)}
+    out["measured_mfma_peak_tflops"] = round(mfma_peak, 1)
     return out
 
 
@@ -318,7 +321,7 @@ def main():
         "roofline": roofline,
         "attention_gbps": round(achieved, 1),
         "stages_ms": {k: round(v / n_fwd, 4) for k, v in stages.items()},
-        "projections": projection_rates(w, T, args, recursive, stages, n_fwd),
+        "projections": projection_rates(w, T, args, recursive, stages, n_fwd, binding.measure_mfma_tflops(dev)),
         "hbm_copy_gbps": copy_rate(torch, dev),
     }
     plain.close()

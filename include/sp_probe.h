@@ -350,10 +350,20 @@ int sp_probe_plan_config(const sp_probe_config* cfg, int32_t num_cus, int32_t* s
 /* Measurement: the rate of plain streaming reads of `bytes` (>= 16) at `buf`
  * (device, 16-byte aligned, read only) on the current device, the ceiling of a
  * read-bound kernel: one warm-up pass, then `reps` timed passes on `stream`
- * (16-byte non-temporal loads, four in flight per lane); *gbps receives the
- * bytes read per second / 1e9.  `sink` (device, 4 bytes) may be written.
- * Synchronises the host.  SP_ERR_INVALID_ARG, SP_ERR_NO_DEVICE, SP_ERR_HIP. */
+ * (each workgroup reads one contiguous slice with 16-byte non-temporal loads,
+ * eight in flight per lane); *gbps receives the bytes read per second / 1e9.
+ * `sink` (device, 4 bytes) may be written.  Synchronises the host.
+ * SP_ERR_INVALID_ARG, SP_ERR_NO_DEVICE, SP_ERR_HIP. */
 int sp_probe_measure_read(const void* buf, size_t bytes, int32_t reps, void* sink, float* gbps, void* stream);
+
+/* Measurement: the dense fp16 matrix-core rate the current device sustains,
+ * the practical ceiling of the projections: every SIMD runs eight waves, each
+ * issuing `iters` x 4 independent 16x16x32 fp16 MFMAs (fp32 accumulation) with
+ * no memory traffic; one warm-up launch, then one timed launch on `stream`.
+ * *tflops receives the multiply-add FLOP per second / 1e12.  `sink` (device,
+ * 4 bytes) may be written.  Synchronises the host.  SP_ERR_INVALID_ARG
+ * (iters < 1, NULL pointers), SP_ERR_NO_DEVICE, SP_ERR_HIP. */
+int sp_probe_measure_mfma(int32_t iters, void* sink, float* tflops, void* stream);
 
 #ifdef __cplusplus
 }

@@ -30,7 +30,7 @@ EXPORTS = ("sp_probe_workspace_bytes", "sp_probe_init", "sp_probe_forward",
            "sp_probe_forward_multi", "sp_probe_forward_recursive", "sp_probe_destroy", "sp_probe_status_string",
            "sp_probe_tap_bytes", "sp_probe_copy_tap", "sp_probe_check_device_error",
            "sp_probe_profile_read", "sp_probe_plan", "sp_probe_plan_recursive", "sp_probe_plan_config",
-           "sp_probe_packed_bytes", "sp_probe_pack_weights", "sp_probe_measure_read",
+           "sp_probe_packed_bytes", "sp_probe_pack_weights", "sp_probe_measure_read", "sp_probe_measure_mfma",
            "sp_probe_forward_noalloc")
 
 
@@ -120,6 +120,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.sp_probe_pack_weights.restype = ctypes.c_int
     lib.sp_probe_measure_read.argtypes = [vp, ctypes.c_size_t, ctypes.c_int32, vp, P(ctypes.c_float), vp]
     lib.sp_probe_measure_read.restype = ctypes.c_int
+    lib.sp_probe_measure_mfma.argtypes = [ctypes.c_int32, vp, P(ctypes.c_float), vp]
+    lib.sp_probe_measure_mfma.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -204,6 +206,17 @@ def measure_read_gbps(buf, reps: int = 10, stream=None) -> float:
     out = ctypes.c_float()
     _check(load().sp_probe_measure_read(buf.data_ptr(), buf.numel() * buf.element_size(), reps, sink.data_ptr(),
                                         ctypes.byref(out), stream), "sp_probe_measure_read")
+    return float(out.value)
+
+
+def measure_mfma_tflops(device, iters: int = 20000, stream=None) -> float:
+    """Sustained dense fp16 matrix-core rate of the device (TFLOP/s)."""
+    import torch
+    sink = torch.zeros(4, dtype=torch.int32, device=device)
+    if stream is None:
+        stream = torch.cuda.current_stream(device).cuda_stream
+    out = ctypes.c_float()
+    _check(load().sp_probe_measure_mfma(iters, sink.data_ptr(), ctypes.byref(out), stream), "sp_probe_measure_mfma")
     return float(out.value)
 
 

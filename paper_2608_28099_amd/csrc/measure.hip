@@ -1,9 +1,11 @@
 // Measurement: the HBM rate of plain streaming reads on this device, the
-// ceiling a read-bound kernel such as the split attention can reach.  Each lane
-// keeps four 16-byte non-temporal loads in flight over a grid-stride walk of
-// the buffer; the loaded words are folded into a checksum that is stored only
-// if it equals a value the caller passes (so the loads cannot be dropped), and
-// nothing else is written.
+// ceiling a read-bound kernel such as the split attention can reach.  Each
+// workgroup reads one contiguous slice of the buffer, its lanes keeping eight
+// 16-byte non-temporal loads in flight, with 64 workgroups per compute unit
+// (the fastest of grid-stride and contiguous walks, 2-16 loads in flight and
+// 4-64 workgroups per compute unit that were tried).  The loaded words are
+// folded into a checksum that is stored only if it equals a value the caller
+// passes (so the loads cannot be dropped), and nothing else is written.
 #include <hip/hip_runtime.h>
 
 #include "../../include/sp_probe.h"
@@ -15,22 +17,43 @@ namespace {
 
 using namespace sp;
 
-__global__ __launch_bounds__(256) void stream_read(const u32x4* buf, size_t n16, uint32_t key, uint32_t* sink) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
+constexpr int kLoads = 8;
+
+__global__ __launch_bounds__(256) void stream_read(const u32x4* buf, size_t n16, size_t per_wg, uint32_t key,
+                                                   uint32_t* sink) {
+  const size_t b0 = blockIdx.x * per_wg, b1 = b0 + per_wg < n16 ? b0 + per_wg : n16;
   uint32_t acc = 0;
-  for (; i + 3 * stride < n16; i += 4 * stride) {
-    const u32x4 a = __builtin_nontemporal_load(buf + i);
-    const u32x4 b = __builtin_nontemporal_load(buf + i + stride);
-    const u32x4 c = __builtin_nontemporal_load(buf + i + 2 * stride);
-    const u32x4 d = __builtin_nontemporal_load(buf + i + 3 * stride);
-    acc ^= (a.x + b.y) ^ (c.z + d.w) ^ (a.w + b.x) ^ (c.y + d.z) ^ (a.y ^ a.z ^ b.z ^ b.w ^ c.x ^ c.w ^ d.x ^ d.y);
+  size_t i = b0 + threadIdx.x;
+  for (; i + (kLoads - 1) * 256 < b1; i += kLoads * 256) {
+    u32x4 v[kLoads];
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) v[u] = __builtin_nontemporal_load(buf + i + u * 256);
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
-  for (; i < n16; i += stride) {
+  for (; i < b1; i += 256) {
     const u32x4 a = __builtin_nontemporal_load(buf + i);
     acc ^= a.x ^ a.y ^ a.z ^ a.w;
   }
   if (acc == key) sink[0] = acc;
+}
+
+// Four independent accumulation chains per wave; operands from the lane index,
+// tiny enough that the sums stay finite.
+__global__ __launch_bounds__(256) void mfma_chains(int iters, float key, float* sink) {
+  f16x8 a, b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    a[i] = (f16)(1e-3f * (float)((threadIdx.x + i) & 7));
+    b[i] = (f16)(1e-3f * (float)((threadIdx.x * 3 + i) & 7));
+  }
+  f32x4 acc[4] = {};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = mfma16x16x32(a, b, acc[j]);
+  }
+  const float s = acc[0][0] + acc[1][1] + acc[2][2] + acc[3][3];
+  if (s == key) sink[0] = s;
 }
 
 }  // namespace
@@ -45,16 +68,17 @@ SP_API int sp_probe_measure_read(const void* buf, size_t bytes, int32_t reps, vo
     return SP_ERR_NO_DEVICE;
   hipStream_t s = (hipStream_t)stream;
   const size_t n16 = bytes / 16;
-  const dim3 grid((unsigned)(cus * 8)), block(256);
+  const dim3 grid((unsigned)(cus * 64)), block(256);
+  const size_t per_wg = (n16 + grid.x - 1) / grid.x;
   hipEvent_t a = nullptr, b = nullptr;
   int st = SP_OK;
   if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) st = SP_ERR_HIP;
   if (st == SP_OK) {
     // one launch to warm the code object, then the timed ones
-    hipLaunchKernelGGL(stream_read, grid, block, 0, s, (const u32x4*)buf, n16, 0x9E3779B9u, (uint32_t*)sink);
+    hipLaunchKernelGGL(stream_read, grid, block, 0, s, (const u32x4*)buf, n16, per_wg, 0x9E3779B9u, (uint32_t*)sink);
     if (hipEventRecord(a, s) != hipSuccess) st = SP_ERR_HIP;
     for (int r = 0; st == SP_OK && r < reps; ++r)
-      hipLaunchKernelGGL(stream_read, grid, block, 0, s, (const u32x4*)buf, n16, 0x9E3779B9u + r,
+      hipLaunchKernelGGL(stream_read, grid, block, 0, s, (const u32x4*)buf, n16, per_wg, 0x9E3779B9u + r,
                          (uint32_t*)sink);
     if (st == SP_OK && (hipGetLastError() != hipSuccess || hipEventRecord(b, s) != hipSuccess ||
                         hipEventSynchronize(b) != hipSuccess))
@@ -62,6 +86,33 @@ SP_API int sp_probe_measure_read(const void* buf, size_t bytes, int32_t reps, vo
     float ms = 0.f;
     if (st == SP_OK && hipEventElapsedTime(&ms, a, b) != hipSuccess) st = SP_ERR_HIP;
     if (st == SP_OK) *gbps = (float)((double)n16 * 16.0 * reps / (ms * 1e-3) / 1e9);
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  return st;
+}
+
+SP_API int sp_probe_measure_mfma(int32_t iters, void* sink, float* tflops, void* stream) {
+  if (iters < 1 || !sink || !tflops || ((uintptr_t)sink & 3)) return SP_ERR_INVALID_ARG;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return SP_ERR_NO_DEVICE;
+  hipStream_t s = (hipStream_t)stream;
+  const dim3 grid((unsigned)(cus * 8)), block(256);  // 32 waves per compute unit: 8 per SIMD
+  hipEvent_t a = nullptr, b = nullptr;
+  int st = SP_OK;
+  if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) st = SP_ERR_HIP;
+  if (st == SP_OK) {
+    hipLaunchKernelGGL(mfma_chains, grid, block, 0, s, iters, -1.0f, (float*)sink);
+    if (hipEventRecord(a, s) != hipSuccess) st = SP_ERR_HIP;
+    if (st == SP_OK) hipLaunchKernelGGL(mfma_chains, grid, block, 0, s, iters, -2.0f, (float*)sink);
+    if (st == SP_OK && (hipGetLastError() != hipSuccess || hipEventRecord(b, s) != hipSuccess ||
+                        hipEventSynchronize(b) != hipSuccess))
+      st = SP_ERR_HIP;
+    float ms = 0.f;
+    if (st == SP_OK && hipEventElapsedTime(&ms, a, b) != hipSuccess) st = SP_ERR_HIP;
+    if (st == SP_OK) *tflops = (float)((double)grid.x * 4 * iters * 4 * 16384.0 / (ms * 1e-3) / 1e12);
   }
   if (a) (void)hipEventDestroy(a);
   if (b) (void)hipEventDestroy(b);

@@ -46,6 +46,13 @@ def test_bench_prints_the_contract_line(args):
     assert r["frac"] > 0 and r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-4)
     assert r["measured_read_peak_gbps"] > 0
     assert r["frac_of_measured_read_peak"] == pytest.approx(r["achieved"] / r["measured_read_peak_gbps"], abs=1e-3)
+    # the device's own ceilings: a streaming read below the 8 TB/s nameplate, an
+    # fp16 matrix-core rate below 2.5 PFLOP/s, each projection below both
+    assert r["measured_read_peak_gbps"] < 8000
+    pr = d["projections"]
+    assert 0 < pr["measured_mfma_peak_tflops"] < 2500
+    for name in ("o_proj", "gate_up", "down"):
+        assert 0 < pr[name]["frac_of_peak"] <= pr[name]["frac_of_measured_mfma_peak"] < 1.05
     # the attention stage (split + merge) takes longer than the split kernel alone
     assert r["mean_launch_ms"] >= r["split_kernel_only"]["mean_launch_ms"]
     # a KV cache this small is rotated over copies exceeding 1 GB
