@@ -41,8 +41,9 @@ HBM_PEAK_GBPS = 8000.0
 MFMA_PEAK_TFLOPS = 2500.0   # dense fp16 / bf16 matrix-core peak
 DEFAULT_WORKLOAD = {"one-pass": "long_9b_bf16", "recursive": "long_9b_bf16_sp5"}
 DTYPE_LABEL = {"bf16": "bf16 storage; fp16xfp16->fp32 MFMA projections (fp16 image of the bf16 weights); "
-                       "bf16 MFMA attention on stored K/V with hi+lo bf16 queries and probabilities; "
-                       "fp32 softmax, norms, residual stream and logits",
+                       "attention on the stored bf16 K/V: bf16 MFMA with hi+lo bf16 queries and probabilities "
+                       "up to 6 query tiles per KV head, fp16 MFMA (K/V converted in LDS) from 7; soft keys as "
+                       "hi+lo bf16 MFMA products; fp32 softmax, norms, residual stream and logits",
                "f32": "f32"}
 ROTATE_BELOW = 1 << 30      # KV caches smaller than this are rotated over copies
 ATTN_SRCS = [os.path.join(ROOT, "paper_2608_28099_amd", "csrc", f) for f in ("attention.hip", "merge.hip")]
@@ -308,7 +309,7 @@ def main():
         "value": round(w.batch * T / (ms_per_step * 1e-3), 1), "unit": "classifications/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": DTYPE_LABEL[w.dtype],
-        "data": "synthetic (seeded; random-init head weights; paged KV ~N(0,1))",
+        "data": f"synthetic (seeded; random-init head weights; {w.layout} KV ~N(0,1))",
         "config": {"workload": w.name, "batch": w.batch, "seq_len": list(w.seq_len), "k": w.k,
                    "hidden": w.hidden, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads,
                    "head_dim": w.head_dim, "intermediate": w.intermediate, "n_classes": w.n_classes,
