@@ -180,8 +180,9 @@ def test_merge_rows_per_workgroup(dev):
 def test_projection_tile_shapes(dev):
     """Shapes whose projections select the fallback tiles of the bf16 GEMM:
     64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, the
-    32-deep K step (width 4128 is not a multiple of 64) with head_dim 64, and
-    the split-K 256x128 tile of a deep down projection."""
+    32-deep K step (width 4128 is not a multiple of 64) with head_dim 64, the
+    split-K 256x128 tile of a deep down projection, and the double-buffered
+    256x256 gate/up tile on 304 rows (a second row tile of 48 rows)."""
     cases = [
         configs.Workload(name="tiles_a", dtype="bf16", batch=16, k=16, hidden=4096, n_q_heads=8,
                          n_kv_heads=2, head_dim=128, intermediate=1024, n_classes=3,
@@ -193,6 +194,10 @@ def test_projection_tile_shapes(dev):
         configs.Workload(name="tiles_c", dtype="bf16", batch=9, k=16, hidden=512, n_q_heads=8,
                          n_kv_heads=2, head_dim=64, intermediate=8192, n_classes=2,
                          seq_len=("uniform", 0, 700), seed=52),
+        # 304 rows, gate/up 1280 wide: 256 x 256 tiles in 64-deep double-buffered steps
+        configs.Workload(name="tiles_d", dtype="bf16", batch=19, k=16, hidden=512, n_q_heads=8,
+                         n_kv_heads=2, head_dim=64, intermediate=640, n_classes=2,
+                         seq_len=("uniform", 0, 400), seed=53),
     ]
     for w in cases:
         announce(f"[tiles] {w.name}")
