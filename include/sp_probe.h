@@ -54,8 +54,9 @@ typedef enum sp_status {
                                 id, class row or weight-image header */
   SP_ERR_RANGE = -8,         /* reported by sp_probe_check_device_error: an fp16 activation
                                 (normed row, attention output, SwiGLU product) exceeded 65504 */
-  SP_ERR_INTERNAL = -9       /* reported by sp_probe_check_device_error: a guard word between
-                                workspace areas was overwritten (a library fault) */
+  SP_ERR_INTERNAL = -9       /* a library fault: reported by sp_probe_check_device_error when a
+                                guard word between workspace areas was overwritten, or returned
+                                by a forward whose plan does not fit the handle's workspace */
 } sp_status;
 
 typedef enum sp_dtype {

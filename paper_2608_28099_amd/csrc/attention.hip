@@ -329,15 +329,22 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
   // run on one XCD at about the same time.  With the split index fastest,
   // the splits past the end of short sequences (which exit at once) would all
   // fall on the same XCDs.
-  const int s = blockIdx.y;
   const int g = blockIdx.x % p.n_kv, qg = blockIdx.x / p.n_kv;
-  // sequence slots run longest sequence first: the longest splits start in the
-  // first round and the short ones fill the end of the launch
-  const int b = p.order ? __builtin_amdgcn_readfirstlane(p.order[blockIdx.z]) : blockIdx.z;
+  // Work item of this slot: from the work list (longest items first, so the
+  // short ones fill the end of the launch, and no slot lands on a split past
+  // the end of its sequence), else (sequence z, split y).
+  int b = blockIdx.z, s = blockIdx.y;
+  if (p.items) {
+    const int L = blockIdx.y + blockIdx.z * gridDim.y;
+    if (L >= *p.n_items) return;
+    const int2 it = p.items[L];
+    b = __builtin_amdgcn_readfirstlane(it.x);
+    s = __builtin_amdgcn_readfirstlane(it.y);
+  }
   if (p.err && *p.err) return;
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int t0 = s * p.split_len;
-  if (s > 0 && t0 >= n) return;
+  if (s > 0 && t0 >= n) return;  // (only without the work list)
   const int t1 = min(n, t0 + p.split_len);
   // this wave's query tiles: [tb, tb + ntw) of the group's n_tiles (one each
   // when TPW = 1, else an even share of at most TPW)
@@ -564,7 +571,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
   if (p.err && *p.err) return;
   const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
   const int t0 = s * p.split_len;
-  if (s > 0 && t0 >= n) return;
+  if (s > 0 && t0 >= n) return;  // (only without the work list)
   const int t1 = min(n, t0 + p.split_len);
   const int R = p.rows;
   const int bs = 1 << p.bs_log2;
@@ -644,26 +651,63 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
   }
 }
 
-// One workgroup: the rank of each sequence by clamped length, longest first,
-// ties by index (a deterministic permutation).
-__global__ __launch_bounds__(1024) void order_by_length(const int* seq_lens, int batch, int max_seq_len,
-                                                        int* order) {
-  for (int b = threadIdx.x; b < batch; b += blockDim.x) {
-    const int nb = clamp_len(seq_lens, b, max_seq_len);
-    int rank = 0;
-    for (int o = 0; o < batch; ++o) {
-      const int no = clamp_len(seq_lens, o, max_seq_len);
-      rank += (no > nb) || (no == nb && o < b);
+// One workgroup of 1024 threads: the work list (see launch_work_list).  Full
+// splits: an exclusive scan of (splits - 1) per sequence, 1024 sequences at a
+// time; last splits: the rank of each by (tokens descending, sequence), the
+// candidates staged 1024 at a time in LDS.
+__global__ __launch_bounds__(1024) void work_list(const int* seq_lens, int batch, int max_seq_len, int split_len,
+                                                  int2* items, int* count) {
+  __shared__ int scan[1024];
+  __shared__ int carry;
+  const int tid = threadIdx.x;
+  auto splits = [&](int b) { const int n = clamp_len(seq_lens, b, max_seq_len); return n > 0 ? (n + split_len - 1) / split_len : 1; };
+  auto last_tokens = [&](int b) { const int n = clamp_len(seq_lens, b, max_seq_len); return n - (splits(b) - 1) * split_len; };
+  if (tid == 0) carry = 0;
+  __syncthreads();
+  for (int b0 = 0; b0 < batch; b0 += 1024) {
+    const int b = b0 + tid;
+    const int nf = b < batch ? splits(b) - 1 : 0;
+    scan[tid] = nf;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int v = tid >= o ? scan[tid - o] : 0;
+      __syncthreads();
+      scan[tid] += v;
+      __syncthreads();
     }
-    order[rank] = b;
+    const int off = carry + scan[tid] - nf;
+    for (int sp = 0; sp < nf; ++sp) items[off + sp] = make_int2(b, sp);
+    __syncthreads();
+    if (tid == 1023) carry += scan[1023];
+    __syncthreads();
   }
+  const int full = carry;
+  for (int b0 = 0; b0 < batch; b0 += 1024) {
+    const int b = b0 + tid;
+    const int rb = b < batch ? last_tokens(b) : 0;
+    int rank = 0;
+    for (int o0 = 0; o0 < batch; o0 += 1024) {
+      __syncthreads();
+      scan[tid] = o0 + tid < batch ? last_tokens(o0 + tid) : -1;
+      __syncthreads();
+      const int m = min(1024, batch - o0);
+      for (int j = 0; j < m; ++j) {
+        const int ro = scan[j];
+        rank += (ro > rb) || (ro == rb && o0 + j < b);
+      }
+    }
+    if (b < batch) items[full + rank] = make_int2(b, splits(b) - 1);
+  }
+  if (tid == 0) count[0] = full + batch;
 }
 
 }  // namespace
 
-hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t s) {
+hipError_t launch_work_list(const int* seq_lens, int batch, int max_seq_len, int split_len, int2* items, int* count,
+                            hipStream_t s) {
   if (batch <= 0) return hipSuccess;
-  hipLaunchKernelGGL(order_by_length, dim3(1), dim3(1024), 0, s, seq_lens, batch, max_seq_len, order);
+  if (split_len < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(work_list, dim3(1), dim3(1024), 0, s, seq_lens, batch, max_seq_len, split_len, items, count);
   return hipGetLastError();
 }
 

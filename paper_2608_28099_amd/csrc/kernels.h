@@ -67,7 +67,10 @@ struct AttnParams {
   int64_t k_sb, k_sh, v_sb, v_sh;     // elements
   const int* block_table;  // nullable (contiguous)
   const int* seq_lens;
-  const int* order;        // nullable: sequence of each grid slot (longest first), from launch_order_by_length
+  // nullable (bf16 path: from launch_work_list): the (sequence, split) of grid
+  // slot y + max_splits z, for the first *n_items slots; later slots exit
+  const int2* items;
+  const int* n_items;
   const int* err;          // nullable
   float* o_part;           // [B][n_kv][max_splits][r_alloc][hd] fp32, unnormalised
   float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
@@ -94,9 +97,13 @@ inline int attn_wgs_per_cu(int hd, int waves, int tiles_per_wave = 1) {
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t s);
 // fp32 VALU path: head_dim 64/128, rows <= 64.
 hipError_t launch_attention_f32(const AttnParams& p, int hd, int batch, hipStream_t s);
-// order[r] = the sequence of rank r when the batch is sorted by clamped length,
-// longest first, ties by index (a permutation of 0..batch-1).
-hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t s);
+// The split attention's work items in dispatch order (longest first): every
+// split that is not its sequence's last (split_len tokens each), by sequence
+// and split; then each sequence's last split (split 0 of an empty sequence),
+// by token count descending, ties by sequence.  items holds batch * max_splits
+// pairs (sequence, split); *count receives the number written.
+hipError_t launch_work_list(const int* seq_lens, int batch, int max_seq_len, int split_len, int2* items, int* count,
+                            hipStream_t s);
 
 struct MergeParams {
   const float* o_part;

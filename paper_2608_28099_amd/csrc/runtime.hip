@@ -105,7 +105,8 @@ struct Plan {
   // rows and their inputs
   size_t off_rq, off_rq_lo, off_rks, off_rks_lo, off_rvs, off_rvs_lo, off_rqkv, off_ru, off_rhn,
       off_ren, off_rce, off_rx, off_r3, off_rh0, off_rscale;
-  size_t off_order;               // sequences ordered longest first (int32 [max_batch])
+  size_t off_items, off_n_items;  // the attention's work list ([max_batch][splits] int32 pairs) and its length
+  int items_splits;               // splits per sequence the work list has room for (the largest plan's)
   size_t off_gpart, gpart_bytes;  // split-K partial sums of the small-row projections
   size_t off_guard_tab;           // device table of the guard offsets
   size_t guard_off[kMaxGuards];
@@ -232,10 +233,12 @@ Plan make_plan(const sp_probe_config& c, int num_cus) {
   // split partials: the largest of every plan the handle can run
   size_t part_rows = (size_t)p.rec.max_splits * p.rec.r_alloc;
   p.q_rows = 0;
+  p.items_splits = p.rec.max_splits;
   for (int t = 1; t <= p.max_tasks; ++t) {
     const AttnPlan a = one_pass_plan(c, t, num_cus);
     part_rows = std::max(part_rows, (size_t)a.max_splits * a.r_alloc);
     p.q_rows = std::max(p.q_rows, a.r_alloc);
+    p.items_splits = std::max(p.items_splits, a.max_splits);
   }
 
   const size_t B = (size_t)c.max_batch, M = B * S, d = c.hidden, hd = c.head_dim;
@@ -284,7 +287,8 @@ Plan make_plan(const sp_probe_config& c, int num_cus) {
   p.off_r3 = take(B * 3 * d * e);
   p.off_rh0 = take(B * d * 4);
   p.off_rscale = take(B * 4);
-  p.off_order = take(B * 4);
+  p.off_items = take(B * (size_t)p.items_splits * 8);
+  p.off_n_items = take(4);
   // split-K partials: up to 512 rows of the widest product, and four slices of
   // a hidden-wide product on up to 1024 rows (o and down there split K)
   const size_t widest = std::max({(size_t)2 * c.intermediate, (size_t)p.nqkv, d});
@@ -473,8 +477,9 @@ AttnParams attn_params(const Ctx& x, const AttnPlan& a, const sp_kv_cache* kv,
   ap.num_cus = x.n_cus;
   ap.f16 = a.f16;
   ap.stages = 3;
-  // bf16 path: sequence slots in the order launch_order_by_length wrote
-  ap.order = c.dtype == SP_BF16 ? at<int>(x, x.plan->off_order) : nullptr;
+  // bf16 path: the work list launch_work_list wrote for this plan
+  ap.items = c.dtype == SP_BF16 ? at<int2>(x, x.plan->off_items) : nullptr;
+  ap.n_items = c.dtype == SP_BF16 ? at<int>(x, x.plan->off_n_items) : nullptr;
   return ap;
 }
 
@@ -541,7 +546,7 @@ SP_API const char* sp_probe_status_string(int status) {
     case SP_ERR_CAPACITY: return "SP_ERR_CAPACITY: batch exceeds max_batch, or the workspace exceeds the static scratch";
     case SP_ERR_DEVICE_DATA: return "SP_ERR_DEVICE_DATA: invalid seq_lens, block ids, class rows or weight image on the device";
     case SP_ERR_RANGE: return "SP_ERR_RANGE: an fp16 activation exceeded fp16's range";
-    case SP_ERR_INTERNAL: return "SP_ERR_INTERNAL: a workspace guard word was overwritten";
+    case SP_ERR_INTERNAL: return "SP_ERR_INTERNAL: a workspace guard word was overwritten, or the plan is inconsistent";
   }
   return "unknown status";
 }
@@ -756,12 +761,14 @@ int forward_one_pass(const Ctx& x, const sp_kv_cache* kv, const int32_t* seq_len
   }
   if (!mark()) return SP_ERR_HIP;
 
-  // stage 1: split attention over the cached K/V, longest sequences first
+  // stage 1: split attention over the cached K/V, longest work items first
   const AttnParams ap = attn_params(x, ak, kv, seq_lens, block_table, errp, at<void>(x, pl.off_q),
                                     at<void>(x, pl.off_q_lo), at<float>(x, pl.off_opart),
                                     at<float2>(x, pl.off_ml));
   if (dt == kBF16) {
-    SP_TRY(launch_order_by_length(seq_lens, B, c.max_seq_len, at<int>(x, pl.off_order), s));
+    if (ak.max_splits > pl.items_splits) return SP_ERR_INTERNAL;
+    SP_TRY(launch_work_list(seq_lens, B, c.max_seq_len, ak.split_len, at<int2>(x, pl.off_items),
+                            at<int>(x, pl.off_n_items), s));
     SP_TRY(launch_attention_bf16(ap, hd, ak.waves, B, s));
   } else {
     SP_TRY(launch_attention_f32(ap, hd, B, s));
@@ -931,8 +938,12 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
                                c.rms_eps, status, s));
   }
 
-  // the attention of every step runs its sequence slots longest first
-  if (dt == kBF16) SP_TRY(launch_order_by_length(seq_lens, B, c.max_seq_len, at<int>(x, pl.off_order), s));
+  // the attention of every step runs the same work list, longest items first
+  if (dt == kBF16) {
+    if (pl.rec.max_splits > pl.items_splits) return SP_ERR_INTERNAL;
+    SP_TRY(launch_work_list(seq_lens, B, c.max_seq_len, pl.rec.split_len, at<int2>(x, pl.off_items),
+                            at<int>(x, pl.off_n_items), s));
+  }
 
   for (int t = 0; t < K; ++t) {
     // stage 0: x_t = W_fc[:, :d] RMSNorm(h; gamma_h) + c_t, its RMSNorm, Q/K/V, RoPE at N_b + t

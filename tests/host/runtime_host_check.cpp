@@ -120,7 +120,10 @@ static void attn_common(const AttnParams& p, int hd, int batch, size_t e) {
   if (e == 2) g.range(p.q_lo, rows * hd * e, "attention q_lo");
   g.range(p.o_part, rows * p.max_splits * hd * 4, "attention o_part");
   g.range(p.ml_part, rows * p.max_splits * 8, "attention ml_part");
-  g.range(p.order, (size_t)batch * 4, "attention order");
+  if (p.items) {
+    g.range(p.items, (size_t)batch * p.max_splits * 8, "attention work list");
+    g.range(p.n_items, 4, "attention work-list length");
+  }
 }
 
 hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int batch, hipStream_t) {
@@ -131,9 +134,13 @@ hipError_t launch_attention_bf16(const AttnParams& p, int hd, int waves, int bat
   return hipSuccess;
 }
 
-hipError_t launch_order_by_length(const int* seq_lens, int batch, int max_seq_len, int* order, hipStream_t) {
-  (void)seq_lens; (void)max_seq_len;
-  g.range(order, (size_t)batch * 4, "sequence order");
+hipError_t launch_work_list(const int* seq_lens, int batch, int max_seq_len, int split_len, int2* items, int* count,
+                            hipStream_t) {
+  (void)seq_lens;
+  g.expect(split_len > 0, "work list: split_len");
+  g.range(items, (size_t)batch * ((max_seq_len + split_len - 1) / split_len > 0 ? (max_seq_len + split_len - 1) / split_len : 1) * 8,
+          "work list");
+  g.range(count, 4, "work-list length");
   return hipSuccess;
 }
 
