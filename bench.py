@@ -54,7 +54,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--mode", choices=("one-pass", "recursive"), default="one-pass")
     ap.add_argument("--workload", default=None)
     ap.add_argument("--tasks", type=int, default=1,
