@@ -438,3 +438,24 @@ def test_many_tasks(dev):
                                    None, H.oracle_weights(params), H.head_shape(w))
     for t in range(T):
         H.check_logits(got[:, t], ref[:, t], w.dtype, f"task {t}")
+
+
+def test_work_list_over_many_sequences(dev):
+    """1500 ragged sequences (0-1200 tokens) in 256-token splits: the attention's
+    work list then spans two scan blocks of 1024 sequences and ranks 1500 last
+    splits; every sequence's logits match the oracle (a split dropped or taken
+    twice would change that sequence's)."""
+    w = configs.Workload(name="many_seqs_bf16", dtype="bf16", batch=1500, k=2, hidden=256, n_q_heads=4,
+                         n_kv_heads=2, head_dim=64, intermediate=512, n_classes=2,
+                         seq_len=("uniform", 0, 1200), seed=97)
+    announce(f"[work list] {w.name}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    probe = binding.Probe(w, split_len=256)
+    plan = probe.plan(w.batch)
+    assert plan["split_len"] == 256 and plan["max_splits"] == 5
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    assert probe.check_device_error() == 0
+    probe.close()
+    ref = np.stack([o["logits"] for o in H.oracle_outputs(w, kv, params, range(w.batch))])
+    err = H.check_logits(got, ref, w.dtype, w.name)
+    announce(f"[work list] {w.name}: max err {err:.3e} over {w.batch} sequences")
