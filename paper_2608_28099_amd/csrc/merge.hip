@@ -11,40 +11,29 @@
 namespace sp {
 namespace {
 
-// N consecutive soft operands as stored by rope_scatter (fp32, or bf16 hi + lo
-// parts summed in fp32), N a multiple of 8, with 16-byte loads.
-template <typename TI, int N>
-__device__ __forceinline__ void soft_load_vec(const void* hi, const void* lo, int64_t idx, float (&v)[N]) {
-  if constexpr (sizeof(TI) == 4) {
+// N consecutive fp32 soft operands (N a multiple of 4) with 16-byte loads.
+template <int N>
+__device__ __forceinline__ void soft_load_vec(const float* src, int64_t idx, float (&v)[N]) {
 #pragma unroll
-    for (int i = 0; i < N; i += 4) {
-      const float4 x = *reinterpret_cast<const float4*>((const float*)hi + idx + i);
-      v[i] = x.x; v[i + 1] = x.y; v[i + 2] = x.z; v[i + 3] = x.w;
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < N; i += 8) {
-      const bf16x8 h = *reinterpret_cast<const bf16x8*>((const bf16*)hi + idx + i);
-      const bf16x8 l = *reinterpret_cast<const bf16x8*>((const bf16*)lo + idx + i);
-#pragma unroll
-      for (int t = 0; t < 8; ++t) v[i + t] = (float)h[t] + (float)l[t];
-    }
+  for (int i = 0; i < N; i += 4) {
+    const float4 x = *reinterpret_cast<const float4*>(src + idx + i);
+    v[i] = x.x; v[i + 1] = x.y; v[i + 2] = x.z; v[i + 3] = x.w;
   }
 }
 
-// VALU merge (the fp32 path).  One workgroup per (sequence b, KV head g, block of rw consecutive soft rows
-// with queries of one task): its rows see soft keys [j_lo, j] of their task (at
-// most 64), and the workgroup stages the union, [j_lo, j of its last row], once
-// in LDS as fp32 (keys and values; from the stored operands: fp32, or bf16
-// hi + lo), with 16-byte loads.  Its rw G query rows are dealt to the waves; a
+// VALU merge (the fp32 path).  One workgroup per (sequence b, KV head g, block
+// of rw consecutive soft rows with queries of one task): its rows see soft keys
+// [j_lo, j] of their task (at most 64), and the workgroup stages the union,
+// [j_lo, j of its last row], once in LDS (keys and values), with 16-byte loads.
+// Its rw G query rows are dealt to the waves; a
 // wave's first row's split partials and query are requested before the
 // staging, so the two round trips overlap.  Soft scores are fp32, 16 keys per pass: lane l takes
 // key j_lo + 16 ci + (l & 15) over head dims [(l >> 4) hd/4, +hd/4), and two
 // shuffles add the four dim groups.  Then P V (lane l owns output dims
 // l DPL .. l DPL + DPL - 1, DPL = hd / 64, each key's probability broadcast
 // from its lane), and the splits folded in with a running maximum
-// (log-sum-exp rule), four at a time.  TO: output type; TI: soft operand storage.
-template <typename TO, typename TI, int DPL>
+// (log-sum-exp rule), four at a time.
+template <int DPL>
 __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   constexpr int C = 4;                       // splits per batch of loads
   constexpr int HD = 64 * DPL, DG = HD / 4;  // head dim; dims per lane group in the scores
@@ -84,11 +73,10 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   auto load_row = [&](int r, RowIn& in) __attribute__((always_inline)) {
     load_splits(row_base(r), 0, in);
     const int64_t qo = (((int64_t)b * p.n_kv + g) * p.r_alloc + row_qi(r) * p.group + r % p.group) * HD;
-    soft_load_vec<TI, DG>(p.q, p.q_lo, qo + grp * DG, in.qg);
+    soft_load_vec<DG>((const float*)p.q, qo + grp * DG, in.qg);
   };
   RowIn cur;
   if (wave < nrows) load_row(wave, cur);
-  bool oor = false;
 
   // stage the keys and values of the workgroup's window
   const int64_t ko = (((int64_t)b * p.n_kv + g) * p.ks + j_lo) * HD;                      // [ks][hd]
@@ -97,8 +85,8 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
   float* vs_ = kvs + nk_all * HD;
   for (int e = threadIdx.x * 8; e < nk_all * HD; e += blockDim.x * 8) {
     float kx[8], vx[8];
-    soft_load_vec<TI, 8>(p.k_soft, p.k_soft_lo, ko + e, kx);
-    soft_load_vec<TI, 8>(p.v_soft, p.v_soft_lo, vo + e, vx);
+    soft_load_vec<8>((const float*)p.k_soft, ko + e, kx);
+    soft_load_vec<8>((const float*)p.v_soft, vo + e, vx);
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       ks_[e + t] = kx[t];
@@ -182,18 +170,11 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
     }
     const float inv = 1.0f / L;
     const int h = g * p.group + hq;
-    TO* out = (TO*)p.out + ((int64_t)b * p.out_rows + p.out_off + qi) * ((int64_t)p.n_q * HD) +
-              (int64_t)h * HD + i0;
+    float* out = (float*)p.out + ((int64_t)b * p.out_rows + p.out_off + qi) * ((int64_t)p.n_q * HD) +
+                 (int64_t)h * HD + i0;
 #pragma unroll
-    for (int d = 0; d < DPL; ++d) {
-      out[d] = from_f32<TO>(acc[d] * inv);
-      if constexpr (sizeof(TO) == 2) oor |= !(fabsf(acc[d] * inv) <= 65504.0f);
-    }
+    for (int d = 0; d < DPL; ++d) out[d] = acc[d] * inv;
   }
-  // an fp16 output out of fp16's range (a convex combination of the values,
-  // so only values out of range can cause it)
-  if constexpr (sizeof(TO) == 2)
-    if (__any(oor) && lane == 0 && p.status) atomicOr(p.status, kStatusRange);
 }
 
 // bf16 path: the same merge with the soft-key attention on the matrix cores.
@@ -398,8 +379,8 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t s
   const int rows_wg = q.rw * p.group;
   const dim3 block(64 * (rows_wg < 4 ? rows_wg : 4));
   const size_t lds = (size_t)2 * nk_max * p.hd * sizeof(float);  // its keys and values, fp32
-  if (p.hd == 128) hipLaunchKernelGGL((merge_splits<float, float, 2>), grid, block, lds, s, q);
-  else hipLaunchKernelGGL((merge_splits<float, float, 1>), grid, block, lds, s, q);
+  if (p.hd == 128) hipLaunchKernelGGL(merge_splits<2>, grid, block, lds, s, q);
+  else hipLaunchKernelGGL(merge_splits<1>, grid, block, lds, s, q);
   return hipGetLastError();
 }
 
