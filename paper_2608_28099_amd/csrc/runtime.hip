@@ -176,9 +176,10 @@ AttnPlan attn_plan(const sp_probe_config& c, int rows, int num_cus) {
     // Eight or more tiles per group (the 160 rows of the 27B shape, several
     // tasks): one wave per SIMD, each carrying 2-4 tiles, so every K/V fragment
     // read from LDS serves several tiles, with the K/V tiles converted to fp16
-    // once in LDS and single fp16 products (27B shape: 3.2 ms against 5.0 ms for
-    // ten waves of one tile; hi + lo bf16 products at 2-4 tiles per wave are
-    // matrix-core bound and gain nothing).
+    // once in LDS and single fp16 products (27B shape: 2.7-2.8 ms against 5.0 ms
+    // for ten waves of one tile and 4.8-5.5 ms for eight or five waves of two
+    // tiles, which hold fewer waves per compute unit; hi + lo bf16 products at
+    // 2-4 tiles per wave are matrix-core bound and gain nothing).
     if (w >= 8) {
       a.waves = 4;
       a.f16 = 1;
