@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle sample: sequences are timed until this much CPU time has passed")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="also time the vendor library's GEMM (torch.matmul, fp16) on the projection shapes")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -109,6 +111,38 @@ def projection_rates(w, T, args, recursive, stages, n_fwd, mfma_peak):
                      "frac_of_peak": round(tf / MFMA_PEAK_TFLOPS, 4),
                      "frac_of_measured_mfma_peak": round(tf / mfma_peak, 4)}
     out["measured_mfma_peak_tflops"] = round(mfma_peak, 1)
+    return out
+
+
+def library_gemm_ms(torch, dev, w, rows):
+    """The vendor library's GEMM (torch.matmul on fp16 operands, fp16 output,
+    no fused epilogue) on the projection shapes of `rows` rows, for context
+    only: the forward never calls it.  Median of 10 launches, each after a
+    512 MiB write that evicts the caches, as the forward's weights are
+    evicted between uses."""
+    d, I, qw = w.hidden, w.intermediate, w.n_q_heads * w.head_dim
+    shapes = {"o_proj": (rows, d, qw), "gate_up": (rows, 2 * I, d), "down": (rows, d, I)}
+    junk = torch.empty(128 << 20, dtype=torch.float32, device=dev)
+    out = {}
+    for name, (m, n, k) in shapes.items():
+        a = torch.randn(m, k, device=dev, dtype=torch.float16)
+        b = torch.randn(n, k, device=dev, dtype=torch.float16) * 0.05
+        bt = b.t()
+        c = torch.matmul(a, bt)
+        times = []
+        for _ in range(10):
+            junk.add_(1.0)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            torch.matmul(a, bt, out=c)
+            e1.record()
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1))
+        times.sort()
+        ms = (times[4] + times[5]) / 2
+        out[name] = {"ms": round(ms, 4), "tflops": round(2.0 * m * n * k / (ms * 1e-3) / 1e12, 1)}
+        del a, b, bt, c
+    del junk
     return out
 
 
@@ -325,6 +359,12 @@ def main():
         "projections": projection_rates(w, T, args, recursive, stages, n_fwd, binding.measure_mfma_tflops(dev)),
         "hbm_copy_gbps": copy_rate(torch, dev),
     }
+    if args.library_gemm:
+        rows = w.batch * (w.k if recursive else T * (1 if args.last_row_only else w.k))
+        lib = library_gemm_ms(torch, dev, w, rows)
+        for name, r in lib.items():
+            r["ours_over_library_time"] = round(out["projections"][name]["ms"] / r["ms"], 3)
+        out["projections"]["library_gemm_fp16"] = lib
     plain.close()
     prof.close()
     if not args.no_cpu_baseline:

@@ -305,13 +305,18 @@ hipError_t launch_tile(Epilogue epi, const GemmParams& p, int ksplit, hipStream_
 // per step (32-deep steps load half rows, and with them half cache lines), and
 // more stages measured no faster (SwiGLU, fp16 weights, 8192 x 34816 x 5120:
 // 2.35 ms against 2.59 ms for 256 x 256 in 32-deep steps; 2048 x 24576 x 4096:
-// 0.335 ms against 0.368 ms).
+// 0.335 ms against 0.368 ms).  Index 11 is 256 x 160 in three 52 KB stages, for
+// residual products whose 256 x 256 or 256 x 128 grids end in a partial round
+// (8192 x 5120: 1024 tiles, four whole rounds); index 12 is 256 x 192 with
+// 64-deep steps, double-buffered, for SwiGLU grids of one round (512 x 24576 x
+// 4096: 119 us against 124 us in 32-deep steps).
 struct TileShape { int bm, bn, wgm, wgn, bk; };
-constexpr int kNumTiles = 11;
+constexpr int kNumTiles = 13;
 constexpr TileShape kTiles[kNumTiles] = {
     {256, 256, 2, 4, 32}, {256, 192, 4, 2, 32}, {256, 128, 4, 2, 64}, {128, 64, 4, 2, 64},
     {64, 64, 2, 2, 64},   {32, 64, 1, 2, 64},   {16, 32, 1, 1, 64},  {16, 16, 1, 1, 64},
-    {16, 32, 1, 1, 32},   {32, 128, 1, 4, 64},  {256, 256, 4, 2, 64}};
+    {16, 32, 1, 1, 32},   {32, 128, 1, 4, 64},  {256, 256, 4, 2, 64}, {256, 160, 4, 2, 64},
+    {256, 192, 4, 2, 64}};
 constexpr int kOrderSwiglu[9] = {0, 1, 2, 3, 4, 5, 6, 7, 8};
 constexpr int kOrderResid[9] = {2, 1, 0, 3, 4, 5, 6, 7, 8};
 
@@ -334,6 +339,8 @@ hipError_t launch_tile_index(int c, Epilogue epi, const GemmParams& p, int kspli
     case 8: return launch_tile<16, 32, 1, 1, 8, 32>(epi, p, ksplit, s);
     case 9: return launch_tile<32, 128, 1, 4, 6, 64>(epi, p, ksplit, s);
     case 10: return launch_tile<256, 256, 4, 2, 2, 64>(epi, p, ksplit, s);
+    case 11: return launch_tile<256, 160, 4, 2, 3, 64>(epi, p, ksplit, s);
+    case 12: return launch_tile<256, 192, 4, 2, 2, 64>(epi, p, ksplit, s);
   }
   return hipErrorInvalidValue;
 }
@@ -402,8 +409,12 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
   // often as the 128 x 64 tiles, at the same workgroup count.  Four slices
   // when two would leave at most half the compute units a workgroup, else two
   // (512 x 4096 x 12288, 64 tiles: 82 us against 114 us for two slices;
-  // 1024 x 2560 x 9728, 80 tiles: 88 us against 100 us for four).
-  if (epi != kEpiSwiglu && p.M > 128 && p.M <= 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[2])) {
+  // 1024 x 2560 x 9728, 80 tiles: 88 us against 100 us for four).  Also from
+  // K = 4096 when the 128 x 64 grid would end in a partial round (1024 x 2560 x
+  // 4096, o: 51 us against 68 us for 320 tiles of 128 x 64).
+  const bool part_round3 = ((long)((p.M + 127) / 128) * (p.N / 64)) % cus != 0;
+  if (epi != kEpiSwiglu && p.M > 128 && p.M <= 1024 && (p.K >= 8192 || (p.K >= 4096 && part_round3)) &&
+      tile_ok(p, epi, kTiles[2])) {
     const long tiles = (long)((p.M + 255) / 256) * (p.N / 128);
     const int ks = tiles * 2 <= cus / 2 ? 4 : 2;
     if (p.K % (64 * ks) == 0 && fits(ks)) return launch_tile_index(2, epi, p, ks, s);
@@ -419,24 +430,39 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     while (ks < 8 && tiles * ks < cus) ks *= 2;
     if (p.K / 64 / ks >= 8 && fits(ks)) return launch_tile_index(3, epi, p, ks, s);
   }
-  // SwiGLU (gate/up) on more than 256 rows: the wide tiles, priced by the rounds of workgroups the
-  // grid takes on the compute units (a last partial round costs a whole one)
-  // times the tile's work over its measured relative rate (2048-8192 rows,
-  // fp16 weights).  At 1024 x 19456 x 2560 this takes 256 x 128 (608 tiles,
-  // 0.140 ms) over 256 x 256 (304 tiles: two rounds, the second nearly empty,
-  // 0.154 ms).
-  if (epi == kEpiSwiglu && p.M > 256) {
-    static const int cand[4] = {10, 0, 2, 1};
-    static const double rate[4] = {1.0, 0.91, 0.87, 0.82};
+  // The wide tiles, priced by the rounds of workgroups the grid takes on the
+  // compute units (a last partial round costs a whole one) times the tile's
+  // work over its measured relative rate (2048-8192 rows, fp16 weights).
+  auto cheapest = [&](const int* cand, const double* rate, int n) {
     int best = -1;
     double best_cost = 0.0;
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < n; ++i) {
       const TileShape& t = kTiles[cand[i]];
       if (!tile_ok(p, epi, t)) continue;
       const long tiles = (long)((p.M + t.bm - 1) / t.bm) * (p.N / t.bn);
       const double cost = (double)((tiles + cus - 1) / cus) * t.bm * t.bn / rate[i];
       if (best < 0 || cost < best_cost) { best = cand[i]; best_cost = cost; }
     }
+    return best;
+  };
+  // SwiGLU (gate/up) on more than 256 rows.  At 1024 x 19456 x 2560 this takes
+  // 256 x 128 (608 tiles, 0.140 ms) over 256 x 256 (304 tiles: two rounds, the
+  // second nearly empty, 0.154 ms).
+  if (epi == kEpiSwiglu && p.M > 256) {
+    static const int cand[4] = {10, 0, 2, 12};
+    static const double rate[4] = {1.0, 0.91, 0.87, 0.855};
+    const int best = cheapest(cand, rate, 4);
+    if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
+  }
+  // Residual products on more than 1024 rows whose 256 x 128 grid fills the
+  // compute units: 8192 x 5120 takes 256 x 160 (four whole rounds; o 0.408 ms,
+  // down 1.39 ms) over 256 x 256 (three rounds, the last half empty; 0.413,
+  // 1.40) and 256 x 128 (five rounds; 0.428, 1.43).
+  if (epi != kEpiSwiglu && p.M > 1024 && tile_ok(p, epi, kTiles[2]) &&
+      (long)((p.M + 255) / 256) * (p.N / 128) >= cus) {
+    static const int cand[3] = {10, 11, 2};
+    static const double rate[3] = {1.0, 0.84, 0.80};
+    const int best = cheapest(cand, rate, 3);
     if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
   }
   // First tile (in preference order) that gives at least one workgroup per
