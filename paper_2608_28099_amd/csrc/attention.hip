@@ -657,7 +657,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
 // candidates staged 1024 at a time in LDS.
 __global__ __launch_bounds__(1024) void work_list(const int* seq_lens, int batch, int max_seq_len, int split_len,
                                                   int2* items, int* count) {
-  __shared__ int scan[1024];
+  __shared__ __align__(16) int scan[1024];
   __shared__ int carry;
   const int tid = threadIdx.x;
   auto splits = [&](int b) { const int n = clamp_len(seq_lens, b, max_seq_len); return n > 0 ? (n + split_len - 1) / split_len : 1; };
@@ -688,12 +688,19 @@ __global__ __launch_bounds__(1024) void work_list(const int* seq_lens, int batch
     int rank = 0;
     for (int o0 = 0; o0 < batch; o0 += 1024) {
       __syncthreads();
-      scan[tid] = o0 + tid < batch ? last_tokens(o0 + tid) : -1;
+      scan[tid] = o0 + tid < batch ? last_tokens(o0 + tid) : -1;  // -1: no sequence (ranks below all)
       __syncthreads();
-      const int m = min(1024, batch - o0);
-      for (int j = 0; j < m; ++j) {
-        const int ro = scan[j];
-        rank += (ro > rb) || (ro == rb && o0 + j < b);
+      // four counts per 16-byte LDS read (the slots past the batch hold -1)
+      const int m4 = (min(1024, batch - o0) + 3) / 4;
+      const int4* s4 = (const int4*)scan;
+#pragma unroll 4
+      for (int q = 0; q < m4; ++q) {
+        const int4 r = s4[q];
+        const int j = o0 + 4 * q;
+        rank += (r.x > rb) || (r.x == rb && j < b);
+        rank += (r.y > rb) || (r.y == rb && j + 1 < b);
+        rank += (r.z > rb) || (r.z == rb && j + 2 < b);
+        rank += (r.w > rb) || (r.w == rb && j + 3 < b);
       }
     }
     if (b < batch) items[full + rank] = make_int2(b, splits(b) - 1);

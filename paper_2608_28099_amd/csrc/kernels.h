@@ -48,6 +48,7 @@ struct RopeParams {
   int k_task, q_first, q_per_task;
   double rope_base;
   float q_scale;           // log2(e) / sqrt(hd)
+  int num_cus;             // compute units of the device (sizes the grid)
 };
 // dt: output type: kF32, or kBF16 for the hi/lo bf16 split
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s);

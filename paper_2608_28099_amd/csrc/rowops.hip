@@ -103,68 +103,88 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, c
 }
 
 // ---------------------------------------------------------------- RoPE + scatter
-// One workgroup per (soft row j, sequence b): the rotation of pair (i, i + hd/2)
-// at the row's position N_b + t (t = step + j % k_task) by angle
-// (N_b + t) * base^(-2i/hd) is computed once, in fp64, into LDS, then applied
-// to the row's key heads (soft slot step + j) and, for rows that carry queries,
-// its query heads.  The value heads are not rotated; in the one-pass form
-// (per_seq = 0) they are the same for every sequence and written by b = 0, in
-// the recursive form every sequence has its own row of projections ([B][k]
-// rows) and its own values.
+// One workgroup per (block of up to kRopeRows soft rows j, sequence b): the
+// rotation of pair (i, i + hd/2) at row j's position N_b + t (t = step +
+// j % k_task) by angle (N_b + t) * base^(-2i/hd) is computed once per row, in
+// fp64, into LDS, then applied to the row's key heads (soft slot step + j)
+// and, for rows that carry queries, its query heads, two adjacent pairs per
+// lane (4-byte stores of bf16 pairs, 8-byte of fp32).  The value heads are not
+// rotated; in the one-pass form (per_seq = 0) they are the same for every
+// sequence and written by b = 0, in the recursive form every sequence has its
+// own row of projections ([B][k] rows) and its own values.  Rows per
+// workgroup: as many as keep two workgroups per compute unit (one row each
+// made the 27B-shaped batch 8192 workgroups with a few hundred stores each:
+// 69-76 us, the same with the trigonometry taken out).
 // SPLIT (T = bf16): each value x is stored as hi = bf16(x) and lo = bf16(x - hi).
+constexpr int kRopeRows = 8;
+
 template <typename T, bool SPLIT>
-__device__ __forceinline__ void put(void* hi, void* lo, int64_t idx, float x) {
-  const T h = from_f32<T>(x);
-  ((T*)hi)[idx] = h;
-  if (SPLIT) ((T*)lo)[idx] = from_f32<T>(x - to_f32(h));
+__device__ __forceinline__ void put2(void* hi, void* lo, int64_t idx, float x0, float x1) {  // idx even
+  if constexpr (sizeof(T) == 2) {
+    const T h0 = from_f32<T>(x0), h1 = from_f32<T>(x1);
+    auto pack = [](T a, T b) {
+      return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+    };
+    *(uint32_t*)((T*)hi + idx) = pack(h0, h1);
+    if (SPLIT) *(uint32_t*)((T*)lo + idx) = pack(from_f32<T>(x0 - to_f32(h0)), from_f32<T>(x1 - to_f32(h1)));
+  } else {
+    static_assert(!SPLIT, "fp32 values are stored whole");
+    *(float2*)((T*)hi + idx) = make_float2(x0, x1);
+  }
 }
 
 template <typename T, bool SPLIT>
-__global__ __launch_bounds__(256) void rope_scatter(const RopeParams p) {
-  __shared__ float cs[64], sn[64];  // hd / 2 <= 64
-  const int j = blockIdx.x, b = blockIdx.y;
+__global__ __launch_bounds__(256) void rope_scatter(const RopeParams p, int rows_per_block) {
+  __shared__ float cs[kRopeRows][64], sn[kRopeRows][64];  // hd / 2 <= 64
+  const int b = blockIdx.y, j0 = blockIdx.x * rows_per_block;
   if (p.err && *p.err) return;
-  const int hd = p.hd, half = hd / 2;
+  const int hd = p.hd, half = hd / 2, hp = half / 2;  // hp: lanes per head (two pairs each)
+  const int nj = min(rows_per_block, p.k - j0);
   int n = p.seq_lens[b];
   // a length outside [0, max_seq_len] is clamped (every kernel does the same)
   // and reported through the status word
-  if ((n < 0 || n > p.max_seq_len) && j == 0 && threadIdx.x == 0 && p.status)
+  if ((n < 0 || n > p.max_seq_len) && blockIdx.x == 0 && threadIdx.x == 0 && p.status)
     atomicOr(p.status, kStatusSeqLen);
   n = n < 0 ? 0 : (n > p.max_seq_len ? p.max_seq_len : n);
-  const int jj = j % p.k_task;
-  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+  for (int t = threadIdx.x; t < nj * half; t += blockDim.x) {
+    const int jr = t / half, i = t % half;
+    const int jj = (j0 + jr) % p.k_task;
     const double theta = pow(p.rope_base, -2.0 * (double)i / (double)hd);
     const double ang = (double)(n + p.step + jj) * theta;
-    cs[i] = (float)cos(ang);
-    sn[i] = (float)sin(ang);
+    cs[jr][i] = (float)cos(ang);
+    sn[jr][i] = (float)sin(ang);
   }
   __syncthreads();
-  const int slot = p.step + j;
-  const float* row = p.qkv + ((int64_t)(p.per_seq ? b * p.k : 0) + j) * (p.n_q + 2 * p.n_kv) * hd;
-  const int nrot = (p.n_q + p.n_kv) * half;
-  const int qi = (j / p.k_task) * p.q_per_task + jj - p.q_first;
-  for (int e = jj >= p.q_first ? threadIdx.x : p.n_q * half + threadIdx.x; e < nrot; e += blockDim.x) {
-    const int h = e / half, i = e % half;
-    const float c = cs[i], s = sn[i];
-    const float x0 = row[h * hd + i], x1 = row[h * hd + i + half];
-    const float r0 = x0 * c - x1 * s, r1 = x1 * c + x0 * s;
-    if (h < p.n_q) {
-      const int g = h / p.group, rr = qi * p.group + h % p.group;
-      const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
-      put<T, SPLIT>(p.q, p.q_lo, base + i, r0 * p.q_scale);
-      put<T, SPLIT>(p.q, p.q_lo, base + i + half, r1 * p.q_scale);
-    } else {
-      const int g = h - p.n_q;
-      const int64_t base = (((int64_t)b * p.n_kv + g) * p.ks + slot) * hd;
-      put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i, r0);
-      put<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i + half, r1);
+  const int nh = p.n_q + p.n_kv;
+  for (int jr = 0; jr < nj; ++jr) {
+    const int j = j0 + jr, jj = j % p.k_task, slot = p.step + j;
+    const float* row = p.qkv + ((int64_t)(p.per_seq ? b * p.k : 0) + j) * (p.n_q + 2 * p.n_kv) * hd;
+    const int qi = (j / p.k_task) * p.q_per_task + jj - p.q_first;
+    for (int e = (jj >= p.q_first ? 0 : p.n_q * hp) + threadIdx.x; e < nh * hp; e += blockDim.x) {
+      const int h = e / hp, i = 2 * (e % hp);
+      const float2 xa = *(const float2*)(row + h * hd + i), xb = *(const float2*)(row + h * hd + i + half);
+      const float c0 = cs[jr][i], s0 = sn[jr][i], c1 = cs[jr][i + 1], s1 = sn[jr][i + 1];
+      const float r0a = xa.x * c0 - xb.x * s0, r1a = xb.x * c0 + xa.x * s0;
+      const float r0b = xa.y * c1 - xb.y * s1, r1b = xb.y * c1 + xa.y * s1;
+      if (h < p.n_q) {
+        const int g = h / p.group, rr = qi * p.group + h % p.group;
+        const int64_t base = (((int64_t)b * p.n_kv + g) * p.r_alloc + rr) * hd;
+        put2<T, SPLIT>(p.q, p.q_lo, base + i, r0a * p.q_scale, r0b * p.q_scale);
+        put2<T, SPLIT>(p.q, p.q_lo, base + i + half, r1a * p.q_scale, r1b * p.q_scale);
+      } else {
+        const int g = h - p.n_q;
+        const int64_t base = (((int64_t)b * p.n_kv + g) * p.ks + slot) * hd;
+        put2<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i, r0a, r0b);
+        put2<T, SPLIT>(p.k_soft, p.k_soft_lo, base + i + half, r1a, r1b);
+      }
     }
-  }
-  if (p.per_seq || b == 0) {
-    const int64_t vb = p.per_seq ? (int64_t)b * p.n_kv : 0;
-    for (int e = threadIdx.x; e < p.n_kv * hd; e += blockDim.x) {
-      const int g = e / hd, i = e % hd;
-      put<T, SPLIT>(p.v_soft, p.v_soft_lo, ((vb + g) * p.ks + slot) * hd + i, row[(p.n_q + p.n_kv + g) * hd + i]);
+    if (p.per_seq || b == 0) {
+      const int64_t vb = p.per_seq ? (int64_t)b * p.n_kv : 0;
+      for (int e = threadIdx.x; e < p.n_kv * half; e += blockDim.x) {
+        const int g = e / half, i = 2 * (e % half);
+        const float2 v = *(const float2*)(row + (p.n_q + p.n_kv + g) * hd + i);
+        put2<T, SPLIT>(p.v_soft, p.v_soft_lo, ((vb + g) * p.ks + slot) * hd + i, v.x, v.y);
+      }
     }
   }
 }
@@ -350,12 +370,17 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
 }
 
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s) {
-  if (p.hd > 128) return hipErrorInvalidValue;
-  const dim3 grid(p.k, batch), block(256);
+  if (p.hd > 128 || p.hd % 4 || p.k < 1) return hipErrorInvalidValue;
+  // rows per workgroup: doubled while the grid keeps two workgroups per compute unit
+  const int cus = p.num_cus > 0 ? p.num_cus : 256;
+  int rpb = 1;
+  while (2 * rpb <= kRopeRows && 2 * rpb <= p.k && (int64_t)((p.k + 2 * rpb - 1) / (2 * rpb)) * batch >= 2 * cus)
+    rpb *= 2;
+  const dim3 grid((p.k + rpb - 1) / rpb, batch), block(256);
   if (dt == kBF16)
-    hipLaunchKernelGGL((rope_scatter<bf16, true>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((rope_scatter<bf16, true>), grid, block, 0, s, p, rpb);
   else if (dt == kF32)
-    hipLaunchKernelGGL((rope_scatter<float, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((rope_scatter<float, false>), grid, block, 0, s, p, rpb);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -758,6 +758,7 @@ int forward_one_pass(const Ctx& x, const sp_kv_cache* kv, const int32_t* seq_len
     r.k_task = K; r.q_first = K - Kq; r.q_per_task = Kq;
     r.rope_base = c.rope_base;
     r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
+    r.num_cus = x.n_cus;
     SP_TRY(launch_rope_scatter(dt, r, B, s));
   }
   if (!mark()) return SP_ERR_HIP;
@@ -975,6 +976,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
       r.k_task = 1; r.q_first = 0; r.q_per_task = 1;
       r.rope_base = c.rope_base;
       r.q_scale = (float)(1.4426950408889634 / __builtin_sqrt((double)hd));
+      r.num_cus = x.n_cus;
       SP_TRY(launch_rope_scatter(dt, r, B, s));
     }
     if (!mark()) return SP_ERR_HIP;
