@@ -445,13 +445,16 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     }
     return best;
   };
-  // SwiGLU (gate/up) on 128 rows or more.  At 1024 x 19456 x 2560 this takes
-  // 256 x 128 (608 tiles, 0.140 ms) over 256 x 256 (304 tiles: two rounds, the
-  // second nearly empty, 0.154 ms); at 256 x 34816 x 5120 (last-row-only rows
-  // of the 27B shape) 256 x 256 in one round of 136 tiles (167 us) over 272
-  // tiles of 256 x 128 (197 us); at 128 x 24576 x 4096, 256 x 128 (82 us)
-  // over 128 x 64 (87 us).
-  if (epi == kEpiSwiglu && p.M >= 128) {
+  // SwiGLU (gate/up) on more than 256 rows, and on 128-256 rows when 256 x 128
+  // tiles would fill at least half the compute units (fewer wide tiles would
+  // leave most of them idle; the order below then takes smaller ones).  At
+  // 1024 x 19456 x 2560 this takes 256 x 128 (608 tiles, 0.140 ms) over
+  // 256 x 256 (304 tiles: two rounds, the second nearly empty, 0.154 ms); at
+  // 256 x 34816 x 5120 (last-row-only rows of the 27B shape) 256 x 256 in one
+  // round of 136 tiles (167 us) over 272 tiles of 256 x 128 (197 us); at
+  // 128 x 24576 x 4096, 256 x 128 (82 us) over 128 x 64 (87 us).
+  const long tiles2 = (long)((p.M + 255) / 256) * (p.N / 128);
+  if (epi == kEpiSwiglu && (p.M > 256 || (p.M >= 128 && 2 * tiles2 >= cus))) {
     static const int cand[4] = {10, 0, 2, 12};
     static const double rate[4] = {1.0, 0.91, 0.87, 0.855};
     const int best = cheapest(cand, rate, 4);

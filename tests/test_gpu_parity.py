@@ -114,6 +114,37 @@ def test_soft_row_counts(k, dev):
     probe.close()
 
 
+def test_rope_row_blocks_on_wide_batches(dev):
+    """300 sequences of k = 6 soft rows: the RoPE scatter then takes several
+    rows per workgroup (on a 256-CU device, blocks of 4 and 2 rows), so the
+    per-row angle tables and the paired stores of every block position are
+    checked: attention output and logits against the oracle for every
+    sequence, in the one-pass form and with last-row-only (queries of the
+    last row only)."""
+    w = configs.Workload(name="wide_k6_bf16", dtype="bf16", batch=300, k=6, hidden=256, n_q_heads=4,
+                         n_kv_heads=2, head_dim=64, intermediate=512, n_classes=2,
+                         seq_len=("uniform", 0, 40), layout="paged", seed=61)
+    announce(f"[rope rows] {w.name}")
+    kv, params, kv_d, p_d = small_case(w, dev)
+    outs = H.oracle_outputs(w, kv, params, range(w.batch))
+    ref = np.stack([o["logits"] for o in outs])
+    probe = binding.Probe(w)
+    got = probe.forward(kv_d, p_d).cpu().numpy()
+    attn = probe.tap(binding.SP_TAP_ATTN, w.batch, dev).view(torch.float16).cpu().double().numpy()
+    probe.close()
+    H.check_logits(got, ref, w.dtype, "one-pass")
+    qw = w.n_q_heads * w.head_dim
+    attn = attn.reshape(-1, qw)[: w.batch * w.k].reshape(w.batch, w.k, qw)
+    for b in range(w.batch):
+        o_ref = outs[b]["o"].reshape(w.k, qw)
+        err = np.max(np.abs(attn[b] - o_ref)) / max(np.max(np.abs(o_ref)), 1e-30)
+        assert err < 1e-2, (b, err)
+    lro = binding.Probe(w, flags=binding.SP_FLAG_LAST_ROW_ONLY)
+    got_l = lro.forward(kv_d, p_d).cpu().numpy()
+    lro.close()
+    H.check_logits(got_l, ref, w.dtype, "last-row-only")
+
+
 @pytest.mark.parametrize("hd", [64, 128])
 def test_head_dims_and_splits(hd, dev):
     """Several splits per sequence (split_len 256), head_dim 64 and 128, both dtypes."""
