@@ -212,8 +212,10 @@ def test_projection_tile_shapes(dev):
     """Shapes whose projections select the fallback tiles of the bf16 GEMM:
     64x64 (o-proj, down) and 32x64 (gate/up) at 256 rows x width 4096, the
     32-deep K step (width 4128 is not a multiple of 64) with head_dim 64, the
-    split-K 256x128 tile of a deep down projection, and the double-buffered
-    256x256 gate/up tile on 304 rows (a second row tile of 48 rows)."""
+    split-K 256x128 tile of a deep down projection, the double-buffered
+    256x256 gate/up tile on 304 rows (a second row tile of 48 rows), and the
+    256x160 three-stage tile of the o and down products on 1280 rows x 7680
+    (48 column tiles: one round where 256x128 takes two)."""
     cases = [
         configs.Workload(name="tiles_a", dtype="bf16", batch=16, k=16, hidden=4096, n_q_heads=8,
                          n_kv_heads=2, head_dim=128, intermediate=1024, n_classes=3,
@@ -229,6 +231,10 @@ def test_projection_tile_shapes(dev):
         configs.Workload(name="tiles_d", dtype="bf16", batch=19, k=16, hidden=512, n_q_heads=8,
                          n_kv_heads=2, head_dim=64, intermediate=640, n_classes=2,
                          seq_len=("uniform", 0, 400), seed=53),
+        # 1280 rows, o and down 7680 wide: 256 x 160 tiles
+        configs.Workload(name="tiles_e", dtype="bf16", batch=80, k=16, hidden=7680, n_q_heads=8,
+                         n_kv_heads=2, head_dim=128, intermediate=512, n_classes=2,
+                         seq_len=("uniform", 0, 200), seed=54),
     ]
     for w in cases:
         announce(f"[tiles] {w.name}")
