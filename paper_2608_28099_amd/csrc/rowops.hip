@@ -2,6 +2,7 @@
 // scatter into the attention layouts, final norm + read-out + linear
 // classifier, and the debug validation of device-resident metadata.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -45,20 +46,33 @@ __device__ __forceinline__ void flag_range(bool out_of_range, int* status) {
   if (__any(out_of_range) && (threadIdx.x & 63) == 0 && status) atomicOr(status, kStatusRange);
 }
 
-template <typename TI, typename TG, typename TO>
+// CH: chunks of 1024 values held per row (registers scale with it, so the
+// launcher takes the fewest that cover d).
+template <typename TI, typename TG, typename TO, int CH>
 __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, const TG* gain,
                                                     const TG* gain2, TO* out, int64_t ld_out, int d,
                                                     float eps, int* status) {
+  constexpr int kRowChunks = CH;
   __shared__ float red[4];
   const int r = blockIdx.x;
   const TI* xr = x + (int64_t)r * ld_x;
-  float v[kRowChunks][4];
+  float v[kRowChunks][4], gv[kRowChunks][4];
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < kRowChunks; ++c) {
     const int i = 4 * (threadIdx.x + 256 * c);
+    if (i < d) load4(xr + i, v[c]);
+  }
+  // the gains are loaded under the row's loads and reduction (one round trip, not two)
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int i = 4 * (threadIdx.x + 256 * c);
+    if (i < d) load4(gain + i, gv[c]);
+  }
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int i = 4 * (threadIdx.x + 256 * c);
     if (i < d) {
-      load4(xr + i, v[c]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) ss += v[c][e] * v[c][e];
     }
@@ -67,17 +81,15 @@ __global__ __launch_bounds__(256) void rmsnorm_rows(const TI* x, int64_t ld_x, c
   float inv = 1.0f / sqrtf(ss / (float)d + eps);
   // optional second norm of the result with gain2 (two RMSNorms in a row)
   for (int pass = 0; pass < (gain2 ? 2 : 1); ++pass) {
-    const TG* g = pass ? gain2 : gain;
     float ss2 = 0.f;
 #pragma unroll
     for (int c = 0; c < kRowChunks; ++c) {
       const int i = 4 * (threadIdx.x + 256 * c);
       if (i < d) {
-        float gv[4];
-        load4(g + i, gv);
+        if (pass) load4(gain2 + i, gv[c]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          v[c][e] = v[c][e] * inv * gv[e];
+          v[c][e] = v[c][e] * inv * gv[c][e];
           ss2 += v[c][e] * v[c][e];
         }
       }
@@ -355,18 +367,29 @@ hipError_t launch_rmsnorm_rows(DType in_dt, DType gain_dt, DType out_dt, const v
   if (rows <= 0) return hipSuccess;
   if (d % 4 || d > 1024 * kRowChunks || ld_x % 4 || ld_out % 4) return hipErrorInvalidValue;
   const dim3 grid(rows), block(256);
-  if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
-    hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16>), grid, block, 0, s, (const bf16*)x, ld_x,
-                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
-  else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kF16)
-    hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16>), grid, block, 0, s, (const float*)x, ld_x,
-                       (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
-  else if (in_dt == kF32 && gain_dt == kF32 && out_dt == kF32)
-    hipLaunchKernelGGL((rmsnorm_rows<float, float, float>), grid, block, 0, s, (const float*)x, ld_x,
-                       (const float*)gain, (const float*)gain2, (float*)out, ld_out, d, eps, status);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+  auto run = [&](auto ch) {
+    constexpr int CH = decltype(ch)::value;
+    if (in_dt == kBF16 && gain_dt == kBF16 && out_dt == kF16)
+      hipLaunchKernelGGL((rmsnorm_rows<bf16, bf16, f16, CH>), grid, block, 0, s, (const bf16*)x, ld_x,
+                         (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
+    else if (in_dt == kF32 && gain_dt == kBF16 && out_dt == kF16)
+      hipLaunchKernelGGL((rmsnorm_rows<float, bf16, f16, CH>), grid, block, 0, s, (const float*)x, ld_x,
+                         (const bf16*)gain, (const bf16*)gain2, (f16*)out, ld_out, d, eps, status);
+    else if (in_dt == kF32 && gain_dt == kF32 && out_dt == kF32)
+      hipLaunchKernelGGL((rmsnorm_rows<float, float, float, CH>), grid, block, 0, s, (const float*)x, ld_x,
+                         (const float*)gain, (const float*)gain2, (float*)out, ld_out, d, eps, status);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  };
+  const int ch = (d + 1023) / 1024;
+  if (ch <= 1) return run(std::integral_constant<int, 1>{});
+  if (ch <= 2) return run(std::integral_constant<int, 2>{});
+  if (ch <= 3) return run(std::integral_constant<int, 3>{});
+  if (ch <= 4) return run(std::integral_constant<int, 4>{});
+  if (ch <= 5) return run(std::integral_constant<int, 5>{});
+  if (ch <= 8) return run(std::integral_constant<int, 8>{});
+  return run(std::integral_constant<int, kRowChunks>{});
 }
 
 hipError_t launch_rope_scatter(DType dt, const RopeParams& p, int batch, hipStream_t s) {
