@@ -278,6 +278,58 @@ __global__ __launch_bounds__(256) void gemm_reduce(const GemmParams p, int kspli
   ((float*)p.c)[(int64_t)m * p.ldc + o] = v;
 }
 
+// The same, four consecutive outputs per thread (16-byte partial loads) and
+// one output row per blockIdx.y; the launcher takes it when every row stride
+// and base keeps those accesses aligned.  Same sums in the same order.
+template <int EPI>
+__global__ __launch_bounds__(256) void gemm_reduce4(const GemmParams p, int ksplit, int bn) {
+  const int n_out = EPI == kEpiSwiglu ? p.N / 2 : p.N;
+  const int m = blockIdx.y, o = 4 * (blockIdx.x * 256 + threadIdx.x);
+  if (o >= n_out) return;
+  const int64_t slice = (int64_t)p.M * p.N;
+  const float* src = p.part + (int64_t)m * p.N;
+  if (EPI == kEpiSwiglu) {
+    const int w = o % (bn / 2);  // o % 4 == 0: the four outputs share one 16-column group
+    const int g = (o / (bn / 2)) * bn + 32 * (w / 16) + w % 16;
+    float4 gt = make_float4(0.f, 0.f, 0.f, 0.f), up = gt;
+    for (int k = 0; k < ksplit; ++k) {
+      const float4 a = *reinterpret_cast<const float4*>(src + k * slice + g);
+      const float4 u = *reinterpret_cast<const float4*>(src + k * slice + g + 16);
+      gt.x += a.x; gt.y += a.y; gt.z += a.z; gt.w += a.w;
+      up.x += u.x; up.y += u.y; up.z += u.z; up.w += u.w;
+    }
+    const float v[4] = {silu(gt.x) * up.x, silu(gt.y) * up.y, silu(gt.z) * up.z, silu(gt.w) * up.w};
+    f16x4 h;
+    bool oor = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = (f16)v[e];
+      oor |= !(fabsf(v[e]) <= 65504.0f);
+    }
+    *reinterpret_cast<f16x4*>((f16*)p.c + (int64_t)m * p.ldc + o) = h;
+    if (oor && p.status) atomicOr(p.status, kStatusRange);
+    return;
+  }
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int k = 0; k < ksplit; ++k) {
+    const float4 a = *reinterpret_cast<const float4*>(src + k * slice + o);
+    v.x += a.x; v.y += a.y; v.z += a.z; v.w += a.w;
+  }
+  if (EPI == kEpiResidRow) {
+    const bf16* rr = (const bf16*)p.r + (int64_t)(m % p.r_mod) * p.r_ld + o;
+    v.x += (float)rr[0]; v.y += (float)rr[1]; v.z += (float)rr[2]; v.w += (float)rr[3];
+  }
+  if (EPI == kEpiResidF32) {
+    const float4 r = *reinterpret_cast<const float4*>((const float*)p.r + (int64_t)m * p.r_ld + o);
+    v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+  }
+  if (EPI == kEpiRowScale) {
+    const float sc = ((const float*)p.r)[m];
+    v.x *= sc; v.y *= sc; v.z *= sc; v.w *= sc;
+  }
+  *reinterpret_cast<float4*>((float*)p.c + (int64_t)m * p.ldc + o) = v;
+}
+
 template <int BM, int BN, int WGM, int WGN, int S, int BK, bool PART, bool WB>
 hipError_t launch_tile_k(Epilogue epi, const GemmParams& p, dim3 grid, hipStream_t s) {
   const dim3 block(64 * WGM * WGN);
@@ -365,6 +417,22 @@ hipError_t launch_tile_index(int c, Epilogue epi, const GemmParams& p, int kspli
 
 hipError_t launch_gemm_reduce(Epilogue epi, const GemmParams& p, int ksplit, int bn, hipStream_t s) {
   const int n_out = epi == kEpiSwiglu ? p.N / 2 : p.N;
+  auto al16 = [](const void* q) { return ((uintptr_t)q & 15) == 0; };
+  const bool vec = n_out % 4 == 0 && p.N % 4 == 0 && p.ldc % 4 == 0 && al16(p.part) &&
+                   (epi == kEpiSwiglu ? ((uintptr_t)p.c & 7) == 0 && bn % 32 == 0 : al16(p.c)) &&
+                   (epi == kEpiResidRow ? p.r_ld % 4 == 0 && ((uintptr_t)p.r & 7) == 0 : true) &&
+                   (epi == kEpiResidF32 ? p.r_ld % 4 == 0 && al16(p.r) : true) && p.M <= 65535;
+  if (vec) {
+    const dim3 g4((unsigned)((n_out / 4 + 255) / 256), (unsigned)p.M);
+    switch (epi) {
+      case kEpiStore: hipLaunchKernelGGL(gemm_reduce4<kEpiStore>, g4, dim3(256), 0, s, p, ksplit, bn); break;
+      case kEpiResidRow: hipLaunchKernelGGL(gemm_reduce4<kEpiResidRow>, g4, dim3(256), 0, s, p, ksplit, bn); break;
+      case kEpiResidF32: hipLaunchKernelGGL(gemm_reduce4<kEpiResidF32>, g4, dim3(256), 0, s, p, ksplit, bn); break;
+      case kEpiRowScale: hipLaunchKernelGGL(gemm_reduce4<kEpiRowScale>, g4, dim3(256), 0, s, p, ksplit, bn); break;
+      case kEpiSwiglu: hipLaunchKernelGGL(gemm_reduce4<kEpiSwiglu>, g4, dim3(256), 0, s, p, ksplit, bn); break;
+    }
+    return hipGetLastError();
+  }
   const dim3 rgrid((unsigned)(((int64_t)p.M * n_out + 255) / 256));
   switch (epi) {
     case kEpiStore: hipLaunchKernelGGL(gemm_reduce<kEpiStore>, rgrid, dim3(256), 0, s, p, ksplit, bn); break;
