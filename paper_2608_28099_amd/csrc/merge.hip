@@ -206,6 +206,30 @@ __global__ __launch_bounds__(256) void merge_soft_mfma(const MergeParams p) {
   const int nk_all = p.q_first + p.q_per_task + p.step;  // keys [j_lo, j_lo + nk_all)
   const int nkp = (nk_all + 31) & ~31, ldk = nkp + 4;
 
+  // The lane's query fragments and the first kMl splits' (m, l) are loaded
+  // before the values are staged, so their round trips overlap the staging.
+  const int r = 16 * t + li;               // this lane's query row within the task (column of S^T)
+  const bool valid = t < tiles && r < R;
+  const int rr = valid ? r : R - 1;        // padding columns repeat the last row; never stored
+  const int64_t bg = (int64_t)b * p.n_kv + g;
+  const int64_t qrow = bg * p.r_alloc + (int64_t)task * R + rr;
+  bf16x8 qh[NC], ql[NC];
+  if (t < tiles) {
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qrow * HD + 32 * c + 8 * la));
+      ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qrow * HD + 32 * c + 8 * la));
+    }
+  }
+  constexpr int kMl = 4;
+  const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
+  const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
+  const int64_t base = bg * p.max_splits * p.r_alloc + (int64_t)task * R + rr;
+  float2 ml_pre[kMl];
+#pragma unroll
+  for (int sp = 0; sp < kMl; ++sp)
+    if (t < tiles && sp < ns) ml_pre[sp] = p.ml_part[base + (int64_t)sp * p.r_alloc];
+
   // stage V^T: consecutive lanes take consecutive keys of one 8-dim chunk
   const int64_t vo = (((p.per_seq ? (int64_t)b * p.n_kv : 0) + g) * p.ks + j_lo) * HD;
   for (int e = threadIdx.x; e < nkp * (HD / 8); e += blockDim.x) {
@@ -224,17 +248,6 @@ __global__ __launch_bounds__(256) void merge_soft_mfma(const MergeParams p) {
   __syncthreads();
   if (t >= tiles) return;
 
-  const int r = 16 * t + li;               // this lane's query row within the task (column of S^T)
-  const bool valid = r < R;
-  const int rr = valid ? r : R - 1;        // padding columns repeat the last row; never stored
-  const int64_t bg = (int64_t)b * p.n_kv + g;
-  const int64_t qrow = bg * p.r_alloc + (int64_t)task * R + rr;
-  bf16x8 qh[NC], ql[NC];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    qh[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q + qrow * HD + 32 * c + 8 * la));
-    ql[c] = __builtin_bit_cast(bf16x8, ld16v((const bf16*)p.q_lo + qrow * HD + 32 * c + 8 * la));
-  }
   const int64_t ko = (bg * p.ks + j_lo) * HD;
   const int nkt = (nk_all + 15) >> 4;
   f32x4 sc[4];
@@ -304,19 +317,26 @@ __global__ __launch_bounds__(256) void merge_soft_mfma(const MergeParams p) {
   }
   if (!valid) return;
 
-  // the splits' partials, by the log-sum-exp rule
-  const int n = clamp_len(p.seq_lens, b, p.max_seq_len);
-  const int ns = n > 0 ? (n + p.split_len - 1) / p.split_len : 1;
-  const int64_t base = bg * p.max_splits * p.r_alloc + (int64_t)task * R + r;
+  // the splits' partials, by the log-sum-exp rule (rr == r from here on)
   float Mt = M;
-  for (int sp = 0; sp < ns; ++sp) Mt = fmaxf(Mt, p.ml_part[base + (int64_t)sp * p.r_alloc].x);
+#pragma unroll
+  for (int sp = 0; sp < kMl; ++sp)
+    if (sp < ns) Mt = fmaxf(Mt, ml_pre[sp].x);
+  for (int sp = kMl; sp < ns; ++sp) Mt = fmaxf(Mt, p.ml_part[base + (int64_t)sp * p.r_alloc].x);
   const float a0 = fast_exp2(M - Mt);
   L *= a0;
 #pragma unroll
   for (int dt = 0; dt < NDT; ++dt) o[dt] *= a0;
   for (int sp = 0; sp < ns; ++sp) {
     const int64_t row = base + (int64_t)sp * p.r_alloc;
-    const float2 ml = p.ml_part[row];
+    float2 ml;
+    if (sp < kMl) {
+#pragma unroll
+      for (int q = 0; q < kMl; ++q)
+        if (q == sp) ml = ml_pre[q];
+    } else {
+      ml = p.ml_part[row];
+    }
     const float w = fast_exp2(ml.x - Mt);
     L += ml.y * w;
 #pragma unroll
