@@ -547,10 +547,20 @@ __global__ __launch_bounds__(W * 64) void attn_split_bf16(const AttnParams p) {
     lt += __shfl_xor(lt, 16);
     lt += __shfl_xor(lt, 32);
     if (la == 0) p.ml_part[prow + li] = make_float2(st[t].m, lt);
+    // O / l in fp16: a convex combination of the split's values, so within fp16
+    // whenever V is (the merge weights it by l again); lane (li, la) holds rows
+    // 4la + r, whose sums sit in lanes 4la + r
+    float inv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float lr = __shfl(lt, 4 * la + r);
+      inv[r] = lr > 0.f ? 1.0f / lr : 0.f;
+    }
+    f16* op = (f16*)p.o_part;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) p.o_part[(prow + 4 * la + r) * HD + 16 * nt + li] = st[t].o[nt][r];
+      for (int r = 0; r < 4; ++r) op[(prow + 4 * la + r) * HD + 16 * nt + li] = (f16)(st[t].o[nt][r] * inv[r]);
   }
 }
 
@@ -647,7 +657,7 @@ __global__ __launch_bounds__(256) void attn_split_f32(const AttnParams p) {
   for (int u = 0; u < OPT; ++u) {
     const int idx = tid + 256 * u;
     const int r = idx / HD, i = idx % HD;
-    if (r < R) p.o_part[(prow + r) * HD + i] = oacc[u];
+    if (r < R) ((float*)p.o_part)[(prow + r) * HD + i] = oacc[u];
   }
 }
 

@@ -73,7 +73,10 @@ struct AttnParams {
   const int2* items;
   const int* n_items;
   const int* err;          // nullable
-  float* o_part;           // [B][n_kv][max_splits][r_alloc][hd] fp32, unnormalised
+  // [B][n_kv][max_splits][r_alloc][hd]: bf16 path fp16 O / l (each split's
+  // output normalised by its own sum; 0 for a split with no tokens), fp32 path
+  // fp32 unnormalised O
+  void* o_part;
   float2* ml_part;         // [B][n_kv][max_splits][r_alloc] (running max (log2 units), sum)
   int n_kv, rows, r_alloc, n_qgroups;
   int n_tiles;             // 16-row query tiles per query group (r_alloc = n_qgroups n_tiles 16)
@@ -107,7 +110,7 @@ hipError_t launch_work_list(const int* seq_lens, int batch, int max_seq_len, int
                             hipStream_t s);
 
 struct MergeParams {
-  const float* o_part;
+  const void* o_part;      // as AttnParams::o_part
   const float2* ml_part;
   const int* seq_lens;
   const int* err;

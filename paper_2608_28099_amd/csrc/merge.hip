@@ -67,7 +67,7 @@ __global__ __launch_bounds__(256) void merge_splits(const MergeParams p) {
       const int64_t row = base + (int64_t)min(s0 + c, ns - 1) * p.r_alloc;
       in.ml[c] = p.ml_part[row];
 #pragma unroll
-      for (int d = 0; d < DPL; ++d) in.ov[c][d] = p.o_part[row * HD + i0 + d];
+      for (int d = 0; d < DPL; ++d) in.ov[c][d] = ((const float*)p.o_part)[row * HD + i0 + d];
     }
   };
   auto load_row = [&](int r, RowIn& in) __attribute__((always_inline)) {
@@ -337,12 +337,12 @@ __global__ __launch_bounds__(256) void merge_soft_mfma(const MergeParams p) {
     } else {
       ml = p.ml_part[row];
     }
-    const float w = fast_exp2(ml.x - Mt);
-    L += ml.y * w;
+    const float w = ml.y * fast_exp2(ml.x - Mt);  // the partial is O_s / l_s
+    L += w;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
-      const float4 v = *reinterpret_cast<const float4*>(p.o_part + row * HD + 16 * dt + 4 * la);
-      o[dt] += f32x4{v.x, v.y, v.z, v.w} * w;
+      const f16x4 v = *reinterpret_cast<const f16x4*>((const f16*)p.o_part + row * HD + 16 * dt + 4 * la);
+      o[dt] += f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]} * w;
     }
   }
   const float inv = 1.0f / L;

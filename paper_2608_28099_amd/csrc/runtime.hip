@@ -263,7 +263,7 @@ Plan make_plan(const sp_probe_config& c, int num_cus) {
   p.off_q_lo = take(lo * B * kv * p.q_rows * hd * e);
   p.off_ksoft_lo = take(lo * B * kv * p.ks * hd * e);
   p.off_vsoft_lo = take(lo * kv * hd * p.ks * e);
-  p.off_opart = take(B * kv * part_rows * hd * 4);
+  p.off_opart = take(B * kv * part_rows * hd * e);  // fp16 O / l (bf16 storage) or fp32 O
   p.off_ml = take(B * kv * part_rows * 8);
   p.off_attn = take(M * c.n_q_heads * hd * e);
   p.off_a = take(M * d * 4);
@@ -458,7 +458,7 @@ int check_forward(const sp_probe_config& c, const Plan& pl, const sp_kv_cache* k
 // Split-attention parameters over the caller's cache for one attention plan.
 AttnParams attn_params(const Ctx& x, const AttnPlan& a, const sp_kv_cache* kv,
                        const int32_t* seq_lens, const int32_t* block_table, const int* errp,
-                       const void* q, const void* q_lo, float* o_part, float2* ml_part) {
+                       const void* q, const void* q_lo, void* o_part, float2* ml_part) {
   const sp_probe_config& c = *x.cfg;
   AttnParams ap{};
   ap.q = q;
@@ -765,7 +765,7 @@ int forward_one_pass(const Ctx& x, const sp_kv_cache* kv, const int32_t* seq_len
 
   // stage 1: split attention over the cached K/V, longest work items first
   const AttnParams ap = attn_params(x, ak, kv, seq_lens, block_table, errp, at<void>(x, pl.off_q),
-                                    at<void>(x, pl.off_q_lo), at<float>(x, pl.off_opart),
+                                    at<void>(x, pl.off_q_lo), at<void>(x, pl.off_opart),
                                     at<float2>(x, pl.off_ml));
   if (dt == kBF16) {
     if (ak.max_splits > pl.items_splits) return SP_ERR_INTERNAL;
@@ -983,7 +983,7 @@ SP_API int sp_probe_forward_recursive(sp_probe_t* h, const sp_kv_cache* kv, cons
 
     // stage 1: split attention of the step's G query rows per KV head over the cache
     const AttnParams ap = attn_params(x, rp, kv, seq_lens, block_table, errp, at<void>(x, pl.off_rq),
-                                      at<void>(x, pl.off_rq_lo), at<float>(x, pl.off_opart),
+                                      at<void>(x, pl.off_rq_lo), at<void>(x, pl.off_opart),
                                       at<float2>(x, pl.off_ml));
     if (dt == kBF16)
       SP_TRY(launch_attention_bf16(ap, hd, rp.waves, B, s));

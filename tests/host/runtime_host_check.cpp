@@ -118,7 +118,7 @@ static void attn_common(const AttnParams& p, int hd, int batch, size_t e) {
   const size_t rows = (size_t)batch * p.n_kv * p.r_alloc;
   g.range(p.q, rows * hd * e, "attention q");
   if (e == 2) g.range(p.q_lo, rows * hd * e, "attention q_lo");
-  g.range(p.o_part, rows * p.max_splits * hd * 4, "attention o_part");
+  g.range(p.o_part, rows * p.max_splits * hd * e, "attention o_part");  // fp16 (bf16 path) or fp32
   g.range(p.ml_part, rows * p.max_splits * 8, "attention ml_part");
   if (p.items) {
     g.range(p.items, (size_t)batch * p.max_splits * 8, "attention work list");
@@ -158,7 +158,7 @@ hipError_t launch_merge(DType dt, const MergeParams& p, int batch, hipStream_t) 
   g.expect(p.out_off + p.rows / p.group <= p.out_rows, "merge: output row past out_rows");
   g.expect(p.min_wgs >= 1, "merge: minimum workgroups");
   const size_t rows = (size_t)batch * p.n_kv * p.r_alloc;
-  g.range(p.o_part, rows * p.max_splits * hd * 4, "merge o_part");
+  g.range(p.o_part, rows * p.max_splits * hd * e, "merge o_part");
   g.range(p.ml_part, rows * p.max_splits * 8, "merge ml_part");
   g.range(p.q, rows * hd * e, "merge q");
   g.range(p.k_soft, (size_t)batch * p.n_kv * p.ks * hd * e, "merge k_soft");
