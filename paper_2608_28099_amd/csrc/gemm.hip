@@ -542,12 +542,47 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     static const int cand[4] = {10, 0, 2, 12};
     static const double rate[4] = {1.0, 0.91, 0.87, 0.855};
     const int best = cheapest(cand, rate, 4);
+    // A 256 x 256 grid of more than one round that ends in a partial one: its
+    // whole rounds as 256 x 256 tiles over the first columns, the rest as
+    // 256 x 128 tiles in a second launch (1024 x 19456 x 2560: 124 us against
+    // 137 us for 608 tiles of 256 x 128 and 149 us for 304 of 256 x 256).
+    const int mt = (p.M + 255) / 256, nt = p.N / 256;
+    const long t10 = (long)mt * nt, whole = (t10 / cus) * cus;
+    if (best >= 0 && tile_ok(p, epi, kTiles[10]) && t10 > cus && whole < t10 && whole % mt == 0) {
+      const int na = (int)(whole / mt);            // 256-wide column tiles of the first launch
+      const long tail2 = (long)mt * (nt - na) * 2;  // 256 x 128 tiles of the second
+      const TileShape& tb = kTiles[best];
+      const long tb_tiles = (long)mt * 256 / tb.bm * (p.N / tb.bn);
+      const double split_cost = (double)(whole / cus) * 65536.0 + (double)((tail2 + cus - 1) / cus) * 32768.0 / 0.87;
+      const double best_cost = (double)((tb_tiles + cus - 1) / cus) * tb.bm * tb.bn /
+                               rate[best == 10 ? 0 : best == 0 ? 1 : best == 2 ? 2 : 3];
+      if (split_cost < best_cost) {
+        // output columns [0, 128 na) from the first launch, the rest from the second
+        GemmParams qa = p, qb = p;
+        const int oc = 128 * na;
+        qa.N = 2 * oc;
+        qb.N = p.N - 2 * oc;
+        qb.b[0] = (const uint16_t*)p.b[0] + (int64_t)oc * p.ldb;
+        qb.b[1] = (const uint16_t*)p.b[1] + (int64_t)oc * p.ldb;
+        qb.b[2] = qb.b[1];
+        qb.c = (f16*)p.c + oc;
+        const hipError_t e = launch_tile_index(10, epi, qa, 1, s);
+        return e != hipSuccess ? e : launch_tile_index(2, epi, qb, 1, s);
+      }
+    }
     if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
   }
   // Residual products on more than 1024 rows whose 256 x 128 grid fills the
   // compute units: 8192 x 5120 takes 256 x 160 (four whole rounds; o 0.408 ms,
   // down 1.39 ms) over 256 x 256 (three rounds, the last half empty; 0.413,
   // 1.40) and 256 x 128 (five rounds; 0.428, 1.43).
+  // Long K on more than 1024 rows whose 256 x 256 grid fills at most half the
+  // compute units: those tiles with K split in two (2048 x 4096 x 12288, down:
+  // 201 us against 218 us for 256 tiles of 256 x 128; with K = 4096, o, the
+  // split measured slower).
+  if (epi != kEpiSwiglu && p.M > 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[10]) &&
+      2 * (long)((p.M + 255) / 256) * (p.N / 256) <= cus && p.K % 128 == 0 && fits(2))
+    return launch_tile_index(10, epi, p, 2, s);
   if (epi != kEpiSwiglu && p.M > 1024 && tile_ok(p, epi, kTiles[2]) &&
       (long)((p.M + 255) / 256) * (p.N / 128) >= cus) {
     static const int cand[3] = {10, 11, 2};
