@@ -455,6 +455,45 @@ hipError_t launch_gemm_tile(Epilogue epi, const GemmParams& p, int tile, int ksp
   return launch_tile_index(tile, epi, q, ksplit, s);
 }
 
+// The columns [n1, N) of a product as a product of their own (same rows and
+// K): weights, output and residual offset by n1 columns.  SwiGLU counts n1 in
+// gate and up rows together (n1 / 2 output columns); other epilogues need a
+// single weight block.
+GemmParams columns_from(const GemmParams& p, Epilogue epi, int n1) {
+  GemmParams q = p;
+  q.N = p.N - n1;
+  if (epi == kEpiSwiglu) {
+    const int oc = n1 / 2;
+    q.b[0] = (const uint16_t*)p.b[0] + (int64_t)oc * p.ldb;
+    q.b[1] = (const uint16_t*)p.b[1] + (int64_t)oc * p.ldb;
+    q.b[2] = q.b[1];
+    q.c = (f16*)p.c + oc;
+    return q;
+  }
+  for (int i = 0; i < 3; ++i) q.b[i] = (const uint16_t*)p.b[0] + (int64_t)n1 * p.ldb;
+  q.b_split0 = q.b_split1 = q.N;
+  q.c = (float*)p.c + n1;
+  if (epi == kEpiResidRow) q.r = (const uint16_t*)p.r + n1;
+  if (epi == kEpiResidF32) q.r = (const float*)p.r + n1;
+  return q;
+}
+
+// A grid of 256 x 256 tiles that takes more than one round and ends in a
+// partial one: its whole rounds as 256 x 256 tiles over the first columns (all
+// row tiles of each), the remaining columns as 256 x 128 tiles (rate: their
+// throughput relative to 256 x 256) in a second launch.  Returns the number of
+// 256-wide column tiles of the first launch when that prices cheaper than
+// `other` (rounds x tile area / rate of the single-launch choice), else 0.
+int whole_round_columns(const GemmParams& p, int cus, double other, double rate2) {
+  const int mt = (p.M + 255) / 256, nt = p.N / 256;
+  const long t10 = (long)mt * nt, whole = (t10 / cus) * cus;
+  if (p.N % 256 || t10 <= cus || whole == t10 || whole % mt) return 0;
+  const int na = (int)(whole / mt);
+  const long tail2 = (long)mt * (nt - na) * 2;
+  const double cost = (double)(whole / cus) * 65536.0 + (double)((tail2 + cus - 1) / cus) * 32768.0 / rate2;
+  return cost < other ? na : 0;
+}
+
 hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t s) {
   if (p0.M <= 0) return hipSuccess;
   if (dt == kF32) {
@@ -542,32 +581,18 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     static const int cand[4] = {10, 0, 2, 12};
     static const double rate[4] = {1.0, 0.91, 0.87, 0.855};
     const int best = cheapest(cand, rate, 4);
-    // A 256 x 256 grid of more than one round that ends in a partial one: its
-    // whole rounds as 256 x 256 tiles over the first columns, the rest as
-    // 256 x 128 tiles in a second launch (1024 x 19456 x 2560: 124 us against
-    // 137 us for 608 tiles of 256 x 128 and 149 us for 304 of 256 x 256).
-    const int mt = (p.M + 255) / 256, nt = p.N / 256;
-    const long t10 = (long)mt * nt, whole = (t10 / cus) * cus;
-    if (best >= 0 && tile_ok(p, epi, kTiles[10]) && t10 > cus && whole < t10 && whole % mt == 0) {
-      const int na = (int)(whole / mt);            // 256-wide column tiles of the first launch
-      const long tail2 = (long)mt * (nt - na) * 2;  // 256 x 128 tiles of the second
+    // (1024 x 19456 x 2560: 124 us against 137 us for 608 tiles of 256 x 128
+    // and 149 us for 304 of 256 x 256)
+    if (best >= 0 && tile_ok(p, epi, kTiles[10])) {
       const TileShape& tb = kTiles[best];
-      const long tb_tiles = (long)mt * 256 / tb.bm * (p.N / tb.bn);
-      const double split_cost = (double)(whole / cus) * 65536.0 + (double)((tail2 + cus - 1) / cus) * 32768.0 / 0.87;
-      const double best_cost = (double)((tb_tiles + cus - 1) / cus) * tb.bm * tb.bn /
-                               rate[best == 10 ? 0 : best == 0 ? 1 : best == 2 ? 2 : 3];
-      if (split_cost < best_cost) {
-        // output columns [0, 128 na) from the first launch, the rest from the second
-        GemmParams qa = p, qb = p;
-        const int oc = 128 * na;
-        qa.N = 2 * oc;
-        qb.N = p.N - 2 * oc;
-        qb.b[0] = (const uint16_t*)p.b[0] + (int64_t)oc * p.ldb;
-        qb.b[1] = (const uint16_t*)p.b[1] + (int64_t)oc * p.ldb;
-        qb.b[2] = qb.b[1];
-        qb.c = (f16*)p.c + oc;
+      const long tb_tiles = (long)((p.M + tb.bm - 1) / tb.bm) * (p.N / tb.bn);
+      const int bi = best == 10 ? 0 : best == 0 ? 1 : best == 2 ? 2 : 3;
+      const int na = whole_round_columns(p, cus, (double)((tb_tiles + cus - 1) / cus) * tb.bm * tb.bn / rate[bi], 0.87);
+      if (na > 0) {
+        GemmParams qa = p;
+        qa.N = 256 * na;
         const hipError_t e = launch_tile_index(10, epi, qa, 1, s);
-        return e != hipSuccess ? e : launch_tile_index(2, epi, qb, 1, s);
+        return e != hipSuccess ? e : launch_tile_index(2, epi, columns_from(p, epi, 256 * na), 1, s);
       }
     }
     if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
@@ -583,11 +608,26 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
   if (epi != kEpiSwiglu && p.M > 1024 && p.K >= 8192 && tile_ok(p, epi, kTiles[10]) &&
       2 * (long)((p.M + 255) / 256) * (p.N / 256) <= cus && p.K % 128 == 0 && fits(2))
     return launch_tile_index(10, epi, p, 2, s);
+  // The mixed plan above applies here too (single weight block): 8192 x 5120
+  // as two rounds of 256 x 256 over 4096 columns and one of 256 x 128 over the
+  // last 1024 (down 1.22 ms, o 0.369 ms, against 1.34 and 0.389 for 256 x 160).
   if (epi != kEpiSwiglu && p.M > 1024 && tile_ok(p, epi, kTiles[2]) &&
       (long)((p.M + 255) / 256) * (p.N / 128) >= cus) {
     static const int cand[3] = {10, 11, 2};
     static const double rate[3] = {1.0, 0.84, 0.80};
     const int best = cheapest(cand, rate, 3);
+    if (best >= 0 && tile_ok(p, epi, kTiles[10]) && p.b_split0 >= p.N) {
+      const TileShape& tb = kTiles[best];
+      const long tb_tiles = (long)((p.M + tb.bm - 1) / tb.bm) * (p.N / tb.bn);
+      const int bi = best == 10 ? 0 : best == 11 ? 1 : 2;
+      const int na = whole_round_columns(p, cus, (double)((tb_tiles + cus - 1) / cus) * tb.bm * tb.bn / rate[bi], 0.80);
+      if (na > 0) {
+        GemmParams qa = p;
+        qa.N = qa.b_split0 = qa.b_split1 = 256 * na;
+        const hipError_t e = launch_tile_index(10, epi, qa, 1, s);
+        return e != hipSuccess ? e : launch_tile_index(2, epi, columns_from(p, epi, 256 * na), 1, s);
+      }
+    }
     if (best >= 0) return launch_tile_index(best, epi, p, 1, s);
   }
   // First tile (in preference order) that gives at least one workgroup per

@@ -248,12 +248,14 @@ def test_projection_tile_shapes(dev):
 
 
 def test_projection_split_launches(dev):
-    """The two launch plans that split one projection (on 256 compute units):
+    """The launch plans that split one projection (on 256 compute units):
     gate/up on 272 rows x 2 x 16896 (264 tiles of 256x256, one round and 8 more)
     as 256x256 tiles over its first 16384 output columns and 256x128 tiles over
-    the last 512 in a second launch; and a down projection 8192 deep on 1040
-    rows x 512 as 256x256 tiles with K split in two.  Logits and the residual
-    after the MLP (SP_TAP_Y) against the oracle, row by row."""
+    the last 512 in a second launch; a down projection 8192 deep on 1040 rows x
+    512 as 256x256 tiles with K split in two; and o and down on 2048 rows x 8448
+    (264 tiles of 256x256) as 256x256 tiles over the first 8192 columns and
+    256x128 over the last 256.  Logits and the residuals after the o-projection
+    (SP_TAP_A) and the MLP (SP_TAP_Y) against the oracle, row by row."""
     cases = [
         configs.Workload(name="tiles_f", dtype="bf16", batch=17, k=16, hidden=256, n_q_heads=8,
                          n_kv_heads=2, head_dim=64, intermediate=16896, n_classes=2,
@@ -261,21 +263,25 @@ def test_projection_split_launches(dev):
         configs.Workload(name="tiles_g", dtype="bf16", batch=65, k=16, hidden=512, n_q_heads=8,
                          n_kv_heads=2, head_dim=64, intermediate=8192, n_classes=3,
                          seq_len=("uniform", 0, 150), seed=56),
+        configs.Workload(name="tiles_h", dtype="bf16", batch=128, k=16, hidden=8448, n_q_heads=8,
+                         n_kv_heads=2, head_dim=64, intermediate=256, n_classes=2,
+                         seq_len=("uniform", 0, 100), seed=57),
     ]
     for w in cases:
         announce(f"[split launches] {w.name}")
         kv, params, kv_d, p_d = small_case(w, dev)
         probe = binding.Probe(w)
         got = probe.forward(kv_d, p_d).cpu().numpy()
-        y = probe.tap(binding.SP_TAP_Y, w.batch, dev).view(torch.float32).cpu().double().numpy()
+        taps = {n: probe.tap(t, w.batch, dev).view(torch.float32).cpu().double().numpy().reshape(w.batch, w.k, w.hidden)
+                for n, t in (("a", binding.SP_TAP_A), ("y", binding.SP_TAP_Y))}
         probe.close()
         outs = H.oracle_outputs(w, kv, params, range(w.batch))
         H.check_logits(got, np.stack([o["logits"] for o in outs]), w.dtype, w.name)
-        y = y.reshape(w.batch, w.k, w.hidden)
-        for b in range(w.batch):
-            ref = outs[b]["y"]
-            e = np.max(np.abs(y[b] - ref)) / np.max(np.abs(ref))
-            assert e <= 1e-2, (w.name, b, e)
+        for n, x in taps.items():
+            for b in range(w.batch):
+                ref = outs[b][n]
+                e = np.max(np.abs(x[b] - ref)) / np.max(np.abs(ref))
+                assert e <= 1e-2, (w.name, n, b, e)
 
 
 # ---------------------------------------------------------------- invariances (bitwise)
