@@ -351,7 +351,7 @@ hipError_t launch_tile_k(Epilogue epi, const GemmParams& p, dim3 grid, hipStream
 // K split ksplit ways (ksplit > 1: fp32 partials in p.part, then gemm_reduce).
 template <int BM, int BN, int WGM, int WGN, int S, int BK>
 hipError_t launch_tile(Epilogue epi, const GemmParams& p, int ksplit, hipStream_t s) {
-  if (p.K % (BK * ksplit)) return hipErrorInvalidValue;
+  if (p.K % BK || p.K / BK < ksplit) return hipErrorInvalidValue;  // slices of whole steps, maybe uneven
   const dim3 grid(((p.M + BM - 1) / BM) * (p.N / BN), ksplit);
   hipError_t e;
   if (ksplit > 1)
@@ -527,20 +527,18 @@ hipError_t launch_gemm(DType dt, Epilogue epi, const GemmParams& p0, hipStream_t
     while (ks < 16 && tiles * ks * 2 <= 4 * cus && KT / (ks * 2) >= 8 && fits(ks * 2)) ks *= 2;
     return launch_tile_index(9, epi, p, ks, s);
   }
-  // Long K with a few hundred rows (the down projection of 129-1024 rows):
+  // K of 4096 or more with a few hundred rows (o and down on 129-1024 rows):
   // 256 x 128 tiles with K split re-read the activations and weights half as
-  // often as the 128 x 64 tiles, at the same workgroup count.  Four slices
-  // when two would leave at most half the compute units a workgroup, else two
-  // (512 x 4096 x 12288, 64 tiles: 82 us against 114 us for two slices;
-  // 1024 x 2560 x 9728, 80 tiles: 88 us against 100 us for four).  Also from
-  // K = 4096 when the 128 x 64 grid would end in a partial round (1024 x 2560 x
-  // 4096, o: 51 us against 68 us for 320 tiles of 128 x 64).
-  const bool part_round3 = ((long)((p.M + 127) / 128) * (p.N / 64)) % cus != 0;
-  if (epi != kEpiSwiglu && p.M > 128 && p.M <= 1024 && (p.K >= 8192 || (p.K >= 4096 && part_round3)) &&
-      tile_ok(p, epi, kTiles[2])) {
+  // often as 128 x 64 tiles at the same workgroup count.  As many slices (2-4,
+  // of whole 64-deep steps, not necessarily equal) as keep the grid within one
+  // round (1024 x 2560 x 9728, 80 tiles: 76 us in three slices against 94 us in
+  // two; 1024 x 2560 x 4096: 41 us against 47; 512 x 4096 x 4096, 64 tiles: 38
+  // us in four against 41 us for 256 tiles of 128 x 64; 512 x 4096 x 12288: 77
+  // us in four against 111 us in two).
+  if (epi != kEpiSwiglu && p.M > 128 && p.M <= 1024 && p.K >= 4096 && tile_ok(p, epi, kTiles[2])) {
     const long tiles = (long)((p.M + 255) / 256) * (p.N / 128);
-    const int ks = tiles * 2 <= cus / 2 ? 4 : 2;
-    if (p.K % (64 * ks) == 0 && fits(ks)) return launch_tile_index(2, epi, p, ks, s);
+    const int ks = (int)std::min<long>(4, std::max<long>(2, cus / tiles));
+    if (p.K % 64 == 0 && p.K / 64 >= 8 * ks && fits(ks)) return launch_tile_index(2, epi, p, ks, s);
   }
   // 33..256 rows, epilogues other than SwiGLU (o, down, the fusion products):
   // the weights stream with few tiles, so 128 x 64 tiles with K split until
