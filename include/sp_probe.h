@@ -64,8 +64,9 @@ typedef enum sp_dtype {
   SP_BF16 = 1   /* bf16 storage of weights, soft prompt and KV cache.  Projections: fp16
                    MFMA operands (bf16 weights converted exactly, activations rounded to
                    fp16), fp32 accumulation.  Attention: bf16 MFMA on the stored K and V
-                   with the queries and probabilities split in bf16 hi + lo parts.  fp32
-                   norms, softmax statistics, residual stream and logits.  Range: weight
+                   with the queries and probabilities split in bf16 hi + lo parts; each
+                   split's output is kept as fp16 O/l until the merge.  fp32 norms,
+                   softmax statistics, residual stream and logits.  Range: weight
                    and KV magnitudes must stay below 65504, and so must the fp16
                    activations (normed rows, attention outputs, SwiGLU products: |x| <= 65504);
                    an activation past that is stored as inf and reported by
