@@ -459,7 +459,7 @@ hipError_t launch_gemm_tile(Epilogue epi, const GemmParams& p, int tile, int ksp
 // K): weights, output and residual offset by n1 columns.  SwiGLU counts n1 in
 // gate and up rows together (n1 / 2 output columns); other epilogues need a
 // single weight block.
-GemmParams columns_from(const GemmParams& p, Epilogue epi, int n1) {
+static GemmParams columns_from(const GemmParams& p, Epilogue epi, int n1) {
   GemmParams q = p;
   q.N = p.N - n1;
   if (epi == kEpiSwiglu) {
@@ -484,7 +484,7 @@ GemmParams columns_from(const GemmParams& p, Epilogue epi, int n1) {
 // throughput relative to 256 x 256) in a second launch.  Returns the number of
 // 256-wide column tiles of the first launch when that prices cheaper than
 // `other` (rounds x tile area / rate of the single-launch choice), else 0.
-int whole_round_columns(const GemmParams& p, int cus, double other, double rate2) {
+static int whole_round_columns(const GemmParams& p, int cus, double other, double rate2) {
   const int mt = (p.M + 255) / 256, nt = p.N / 256;
   const long t10 = (long)mt * nt, whole = (t10 / cus) * cus;
   if (p.N % 256 || t10 <= cus || whole == t10 || whole % mt) return 0;
