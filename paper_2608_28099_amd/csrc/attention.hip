@@ -5,8 +5,8 @@
 // query head h = g*G + h%G).  Split s covers cache tokens [s*split_len,
 // min(N_b, (s+1)*split_len)).  Each split keeps an online softmax per row
 // (running max m in log2 units, running sum l, unnormalised output O) and
-// writes it as a partial; the merge (merge.hip) adds the soft keys and
-// combines the partials.
+// writes it as a partial (m, l and, on the bf16 path, O / l in fp16); the
+// merge (merge.hip) adds the soft keys and combines the partials.
 //
 // bf16 path: bf16 KV cache, bf16 MFMA operands, fp32 accumulation.  The two
 // operands the kernel itself rounds, the queries and the probabilities, are

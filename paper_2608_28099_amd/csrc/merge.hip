@@ -5,6 +5,8 @@
 // log-sum-exp rule
 //   M = max(m_soft, max_s m_s),  L = l_soft 2^(m_soft-M) + sum_s l_s 2^(m_s-M),
 //   O = (O_soft 2^(m_soft-M) + sum_s O_s 2^(m_s-M)) / L.
+// The bf16 path's partials hold O_s / l_s in fp16 (O_s = l_s times that); the
+// fp32 path's hold O_s itself.
 #include "common.h"
 #include "kernels.h"
 
